@@ -1,0 +1,156 @@
+"""Seeded synthetic inputs for the GEMM workloads.
+
+This module only draws random numbers and rounds them to the storage type.
+It holds none of the GEMM's arithmetic, so both the GPU library's tests and
+the CPU oracle can read the very same stored operands.
+
+Generator: numpy ``Generator(PCG64(seed))``.  Values are drawn in binary64,
+then rounded to nearest-even into the storage type (fp32 and fp16 by numpy;
+bf16 by rounding to fp32 first and then to bf16 with torch's CPU cast).
+Operands are returned as numpy arrays of the stored bits: float32 for fp32,
+uint16 bit patterns for fp16 and bf16.
+
+Workloads (their shapes follow the paper's dynamic-shape GEMM families, the
+Transformer rows of Table 3 and the BERT GEMM of Section 2.2, stretched to the
+sizes listed below; the paper's own benchmark items are not reproduced):
+
+* ``single_f32``  fp32 77 x 96 x 80, U[-1, 1], seed 0, A drawn before B.
+* ``sweep_f16(M)``  fp16 (M x 768) x (768 x 768), U[-1, 1], seed = M.
+* ``encoder_trial(t)``  bf16, seed t: L ~ U{1..512}, M = 16 L; four GEMMs
+  (M,768)x(768,2304), (M,768)x(768,768), (M,768)x(768,3072),
+  (M,3072)x(3072,768); activations N(0,1), weights N(0,0.02).
+* ``attention_trial(t)``  bf16, seed t: L ~ U{1..1024}, batch 192;
+  S = Q (L x 64) x K^T (64 x L) and O = P (L x L) x V (L x 64); Q, K, V ~ N(0,1);
+  P = row softmax (binary64) of independent N(0,1) logits.
+* ``llm_trial(t)``  bf16, seed t: M = clip(floor(exp(U[0, ln 8193))), 1, 8192);
+  (M,4096)x(4096,4096), (M,4096)x(4096,11008), (M,11008)x(11008,4096);
+  activations N(0,1), weights N(0,0.02).
+* ``small_int`` helpers: integer-valued operands whose every partial sum is
+  exact in fp32 and whose result is exact in the output type.
+"""
+import numpy as np
+
+F32, F16, BF16 = 0, 1, 2
+DTYPES = {"f32": F32, "f16": F16, "bf16": BF16}
+ENCODER_SHAPES = [(768, 2304), (768, 768), (768, 3072), (3072, 768)]   # (K, N) per GEMM
+LLM_SHAPES = [(4096, 4096), (4096, 11008), (11008, 4096)]              # (K, N) per GEMM
+ATTN_BATCH = 16 * 12
+ATTN_HEAD = 64
+
+
+def rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def code_of(dtype):
+    return dtype if isinstance(dtype, int) else DTYPES[dtype]
+
+
+def to_storage(x, dtype):
+    """binary64 values -> stored values (float32 array or uint16 bit patterns)."""
+    code = code_of(dtype)
+    x = np.asarray(x, dtype=np.float64)
+    if code == F32:
+        return x.astype(np.float32)
+    if code == F16:
+        return x.astype(np.float16).view(np.uint16)
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x.astype(np.float32))).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def uniform(g, shape, dtype, lo=-1.0, hi=1.0):
+    return to_storage(g.uniform(lo, hi, size=shape), dtype)
+
+
+def normal(g, shape, dtype, std=1.0):
+    return to_storage(g.normal(0.0, std, size=shape), dtype)
+
+
+def single_f32(seed=0):
+    g = rng(seed)
+    A = uniform(g, (77, 80), F32)
+    B = uniform(g, (80, 96), F32)
+    return A, B
+
+
+def sweep_f16(M, K=768, N=768):
+    g = rng(M)
+    A = uniform(g, (M, K), F16)
+    B = uniform(g, (K, N), F16)
+    return A, B
+
+
+def encoder_shape(t):
+    L = int(rng(t).integers(1, 513))
+    return 16 * L
+
+
+def encoder_trial(t, gemms=(0, 1, 2, 3)):
+    """Returns (M, [(A, B) for each GEMM in ENCODER_SHAPES order])."""
+    g = rng(t)
+    L = int(g.integers(1, 513))
+    M = 16 * L
+    out = []
+    for i, (K, N) in enumerate(ENCODER_SHAPES):
+        A = normal(g, (M, K), BF16, 1.0)
+        B = normal(g, (K, N), BF16, 0.02)
+        if i in gemms:
+            out.append((A, B))
+    return M, out
+
+
+def attention_L(t):
+    return int(rng(t).integers(1, 1025))
+
+
+def attention_trial(t, batch=ATTN_BATCH, d=ATTN_HEAD):
+    """Returns (L, Q, Kt, P, V) with Q [b,L,d], Kt [b,d,L] (materialised K^T),
+    P [b,L,L], V [b,L,d], all bf16 bit patterns, contiguous."""
+    g = rng(t)
+    L = int(g.integers(1, 1025))
+    Q = normal(g, (batch, L, d), BF16)
+    Kmat = g.normal(0.0, 1.0, size=(batch, L, d))
+    Kt = to_storage(np.ascontiguousarray(np.swapaxes(Kmat, 1, 2)), BF16)
+    del Kmat
+    V = normal(g, (batch, L, d), BF16)
+    P = np.empty((batch, L, L), dtype=np.uint16)
+    for b in range(batch):            # one head at a time keeps host memory small
+        z = g.normal(0.0, 1.0, size=(L, L))
+        z -= z.max(axis=1, keepdims=True)
+        e = np.exp(z)
+        P[b] = to_storage(e / e.sum(axis=1, keepdims=True), BF16)
+    return L, Q, Kt, P, V
+
+
+def llm_M(t):
+    u = rng(t).uniform(0.0, np.log(8193.0))
+    return int(min(max(np.floor(np.exp(u)), 1), 8192))
+
+
+def llm_trial(t, gemms=(0, 1, 2)):
+    """Returns (M, [(A, B) per GEMM in LLM_SHAPES order])."""
+    g = rng(t)
+    u = g.uniform(0.0, np.log(8193.0))
+    M = int(min(max(np.floor(np.exp(u)), 1), 8192))
+    out = []
+    for i, (K, N) in enumerate(LLM_SHAPES):
+        A = normal(g, (M, K), BF16, 1.0)
+        B = normal(g, (K, N), BF16, 0.02)
+        if i in gemms:
+            out.append((A, B))
+    return M, out
+
+
+def small_int(g, shape, dtype, lo, hi):
+    """Integers drawn uniformly from [lo, hi] (inclusive), stored exactly."""
+    return to_storage(g.integers(lo, hi + 1, size=shape).astype(np.float64), dtype)
+
+
+def exact_range(K, dtype):
+    """Largest integer magnitude r such that K * r * r stays exactly representable
+    in the output type (11 significand bits fp16, 8 bf16, 24 fp32), so that every
+    partial sum in any order is exact and the output needs no rounding."""
+    p = {F32: 24, F16: 11, BF16: 8}[code_of(dtype)]
+    r = int(np.floor(np.sqrt((2.0 ** p) / max(K, 1))))
+    return max(r, 0)
