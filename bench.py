@@ -1,0 +1,216 @@
+"""Benchmark of the runtime-shaped GEMM path on one MI355X.
+
+Default workload (the dynamic-M sweep): fp16 A (M x 768) x fp16 B (768 x 768),
+fp32 accumulation, fp16 output, for every M in 1..512, inputs U[-1, 1] seeded
+per M (paper_2409_01075_amd.inputs.sweep_f16).  All 512 operand sets are
+resident in HBM before timing (about 1 GB, four times the 256 MB last-level
+cache, so each call reads its operands from HBM rather than from a cache
+warmed by the previous call of the same shape).
+
+One step = one pass over the 512 shapes, one vx_gemm call each, back to back
+on one stream.  A HIP event is recorded on that stream before the first call
+and after every call, so each call's device time is the gap between two
+events.  A short spin kernel is queued ahead of the pass so that the host
+enqueues the whole pass before the device reaches it: the measured times are
+device-side, back-to-back.  The host cost per call (plan lookup + launch) is
+reported separately.
+
+Metric: geometric mean over M of 2*M*N*K / t_M (TFLOP/s), t_M the median over
+the timed steps.  The roofline object describes the kernel that takes the most
+time in the pass: its algorithmic bytes per launch (the compulsory
+(M*K + K*N + M*N)*2 bytes) over its average event-timed duration, against the
+8 TB/s HBM peak (every sweep shape is below the fp16 ridge point of 314.6
+FLOP/byte).  cpu_baseline times the CPU oracle on a bounded subset of the
+same shapes on this host's cores.
+"""
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_TFLOPS = {0: 157.3, 1: 2516.6, 2: 2516.6}
+N_SWEEP, K_SWEEP = 768, 768
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--m-max", type=int, default=512, help="sweep M = 1..m_max")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
+    ap.add_argument("--detail", default=None, help="write per-M results as JSON to this path")
+    return ap.parse_args()
+
+
+def _cpu_threads():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _cpu_baseline(ms, budget_s):
+    """Times the CPU oracle (as it stands) on a bounded subset of the sweep."""
+    import numpy as np
+    import oracle
+    from paper_2409_01075_amd import inputs as I
+    threads = _cpu_threads()
+    done, rates = [], []
+    t_all = time.perf_counter()
+    # every 8th M, in order, until the time budget is used
+    for M in ms[::8]:
+        A, B = I.sweep_f16(M)
+        t0 = time.perf_counter()
+        oracle.gemm(A, B, 1, threads=threads, with_mag=False)
+        dt = time.perf_counter() - t0
+        rates.append(2.0 * M * N_SWEEP * K_SWEEP / dt / 1e12)
+        done.append(M)
+        if time.perf_counter() - t_all > budget_s:
+            break
+    geo = math.exp(sum(math.log(r) for r in rates) / len(rates))
+    return {"value": geo, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "fp16 sweep shapes M in %s (every 8th M from 1, %d shapes, full outputs, "
+                      "fp64 accumulation, decode included), geomean over the sample"
+                      % ("{%d..%d}" % (done[0], done[-1]), len(done))}
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the GEMM path is single-device; "
+              "run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2409_01075_amd import inputs as I
+    from paper_2409_01075_amd import vx
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = vx.lib()
+    ms = list(range(1, args.m_max + 1))
+    N, K = N_SWEEP, K_SWEEP
+
+    # ---- resident inputs
+    sets = []
+    for M in ms:
+        A, B = I.sweep_f16(M, K, N)
+        At = torch.from_numpy(A.view(np.int16)).to(dev).view(torch.float16)
+        Bt = torch.from_numpy(B.view(np.int16)).to(dev).view(torch.float16)
+        Ct = torch.empty((M, N), dtype=torch.float16, device=dev)
+        sets.append((M, At, Bt, Ct))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    calls = [(M, At.data_ptr(), Bt.data_ptr(), Ct.data_ptr()) for (M, At, Bt, Ct) in sets]
+    gemm = L.vx_gemm
+
+    plans = {M: vx.vx_plan_query(1, M, N, K, vx.VX_F16) for M in ms}
+
+    def one_pass(events):
+        for i, (M, a, b, c) in enumerate(calls):
+            st = gemm(M, N, K, 1, a, b, c, sp)
+            if st != 0:
+                raise RuntimeError("vx_gemm M=%d: %s" % (M, vx.STATUS.get(st, st)))
+            if events is not None:
+                events[i + 1].record(stream)
+
+    for _ in range(args.warmup):
+        one_pass(None)
+    torch.cuda.synchronize()
+
+    # host cost per call with cached plans (selector lookup + launch), no events
+    t0 = time.perf_counter()
+    one_pass(None)
+    host_us = (time.perf_counter() - t0) / len(calls) * 1e6
+    torch.cuda.synchronize()
+
+    # spin long enough (about 3x the host enqueue time of a pass) for the host to run ahead
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    torch.cuda._sleep(1000000)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    cycles_per_ms = 1e6 / max(e0.elapsed_time(e1), 1e-3)
+    spin_cycles = int(cycles_per_ms * max(3.0 * host_us * len(calls) * 2 / 1000.0, 2.0))
+
+    per_step = []
+    step_ms = []
+    for s in range(args.steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+        torch.cuda._sleep(spin_cycles)
+        ev[0].record(stream)
+        one_pass(ev)
+        torch.cuda.synchronize()
+        t = [ev[i].elapsed_time(ev[i + 1]) for i in range(len(calls))]   # ms
+        per_step.append(t)
+        step_ms.append(ev[0].elapsed_time(ev[-1]))
+        print("step %d: %.3f ms" % (s, step_ms[-1]), file=sys.stderr, flush=True)
+
+    med = np.median(np.array(per_step), axis=0)        # ms per call, per M
+    flops = np.array([2.0 * M * N * K for M in ms])
+    tflops = flops / (med * 1e-3) / 1e12
+    geo = float(np.exp(np.mean(np.log(tflops))))
+
+    # dominant kernel: the most device time over the pass
+    by_kernel = {}
+    for i, M in enumerate(ms):
+        kid = plans[M].kernel_id
+        d = by_kernel.setdefault(kid, {"t": 0.0, "bytes": 0.0, "flops": 0.0, "n": 0, "ms": []})
+        d["t"] += med[i] * 1e-3
+        d["bytes"] += (M * K + K * N + M * N) * 2.0
+        d["flops"] += flops[i]
+        d["n"] += 1
+        d["ms"].append(M)
+    kid = max(by_kernel, key=lambda k: by_kernel[k]["t"])
+    d = by_kernel[kid]
+    kinfo = vx.vx_registry_get(kid)
+    achieved = d["bytes"] / d["t"] / 1e9          # GB/s
+    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                "kernel": "vxk_%d" % kid,
+                "tile": [kinfo.mb, kinfo.nb, kinfo.kb, kinfo.wm, kinfo.wn, kinfo.mfma_m],
+                "launches_per_step": d["n"], "avg_us": d["t"] / d["n"] * 1e6,
+                "algorithmic_bytes_per_launch": d["bytes"] / d["n"]}
+    # roofline fraction of the whole sweep: t_roof / t_measured per shape (geomean)
+    t_roof = np.maximum(flops / (MFMA_PEAK_TFLOPS[1] * 1e12),
+                        np.array([(M * K + K * N + M * N) * 2.0 for M in ms]) / (HBM_PEAK_GBPS * 1e9))
+    sweep_frac = float(np.exp(np.mean(np.log(t_roof / (med * 1e-3)))))
+
+    out = {
+        "metric": "GEMM TFLOP/s geomean over dynamic-M sweep; % of MFMA/HBM roofline on 1 GPU",
+        "value": geo, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": float(np.median(step_ms)), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "config": {"workload": "dynamic-M sweep: fp16 (M x 768) x (768 x 768), fp32 accumulate, fp16 out, "
+                               "M = 1..%d, U[-1,1] seeded per M; one step = one pass" % args.m_max,
+                   "M": "1..%d" % args.m_max, "N": N, "K": K, "calls_per_step": len(ms)},
+        "roofline": roofline,
+        "sweep_roofline_frac_geomean": sweep_frac,
+        "host_us_per_call": host_us,
+        "kernels_used": len(by_kernel),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = _cpu_baseline(ms, args.cpu_seconds)
+    if args.detail:
+        with open(args.detail, "w") as f:
+            json.dump({"M": ms, "ms": med.tolist(), "tflops": tflops.tolist(),
+                       "kernel": [plans[M].kernel_id for M in ms], "split": [plans[M].split_k for M in ms],
+                       "by_kernel": {str(k): {kk: vv for kk, vv in v.items()} for k, v in by_kernel.items()}},
+                      f)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,185 @@
+/*
+ * vx — runtime-shaped dense GEMM for AMD MI355X (gfx950), C ABI.
+ *
+ * Operation (Section 4.1 of "Vortex: Efficient Sample-Free Dynamic Tensor
+ * Program Optimization via Hardware-aware Strategy Space Hierarchization"):
+ * C = A x B, where M, N and K are known only at call time (Section 2.2).
+ *
+ *   A  M x K, row-major, leading dimension K
+ *   B  K x N, row-major, leading dimension N
+ *   C  M x N, row-major, leading dimension N;   C := A x B  (no alpha/beta)
+ *
+ * A, B and C share one element type (fp32, fp16 or bf16).  Products are
+ * accumulated in fp32 and the result is rounded to nearest-even into C's type.
+ * Each call is served by one of the library's precompiled micro-kernels,
+ * chosen by an analytical cost model of the kernel hierarchy (Section 5.2,
+ * Equations 1-4) from the call's shape and the device's hardware description;
+ * no profiling run and no shape sample is involved.
+ *
+ * Memory: every pointer argument of the GEMM calls is a DEVICE pointer owned
+ * by the caller; the library neither retains nor frees it.  A stream argument
+ * is a hipStream_t passed as void* (NULL = the default stream); the call only
+ * enqueues work on it and returns.  Device-side faults surface at the
+ * caller's next synchronisation of that stream.
+ *
+ * Errors: every function returns a vx_status; nothing throws or aborts.
+ * Argument checks happen before any HIP call, so they also work on a host
+ * without a GPU.
+ *
+ * Threads: all functions may be called concurrently.  Calls that select a
+ * split-K plan share a per-(device, stream) workspace; calls on one stream
+ * are ordered by the stream, so they never race.
+ */
+#ifndef VX_H
+#define VX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { VX_F32 = 0, VX_F16 = 1, VX_BF16 = 2 } vx_dtype;
+
+typedef enum {
+    VX_OK = 0,
+    VX_ERR_INVALID_ARG = 1,       /* negative size/stride, NULL operand with a non-empty extent,
+                                     C overlapping A or B, overlapping C batches */
+    VX_ERR_UNSUPPORTED_DTYPE = 2, /* dtype not one of vx_dtype */
+    VX_ERR_NO_CANDIDATE = 3,      /* no compiled kernel fits (or a forced plan does not exist) */
+    VX_ERR_WORKSPACE = 4,         /* the split-K workspace could not be provided */
+    VX_ERR_HIP = 5                /* a HIP runtime call failed (no device, launch failure, ...) */
+} vx_status;
+
+/* Hardware description that drives candidate feasibility and the cost model
+ * (the GetHardwareInfo step of Algorithm 2).  Filled from hipDeviceProp_t and
+ * a per-architecture table. */
+typedef struct vx_hwinfo {
+    char arch[32];                 /* e.g. "gfx950" */
+    int num_cu;                    /* compute units */
+    int num_xcd;                   /* chiplets; workgroups are dispatched round-robin over them */
+    int simd_per_cu;
+    int wave_size;
+    int max_threads_per_wg;
+    int lds_bytes_per_cu;
+    int vgprs_per_lane;            /* unified VGPR+AGPR file per lane of a SIMD */
+    int max_waves_per_simd;
+    double clock_ghz;              /* peak engine clock */
+    double hbm_gbps;               /* peak HBM bandwidth, GB/s */
+    double l2_bytes_per_xcd;
+    double mall_bytes;             /* last-level (Infinity) cache */
+    double mfma_flop_clk_cu_f16;   /* dense MFMA FLOP per clock per CU, fp16/bf16 inputs */
+    double mfma_flop_clk_cu_f32;   /* dense MFMA FLOP per clock per CU, fp32 inputs */
+    double l2_bytes_clk_cu;        /* L2 -> CU fill rate, bytes per clock */
+    double lds_bytes_clk_cu;       /* LDS read bandwidth per CU, bytes per clock */
+    double mem_latency_ns;         /* global load-to-use latency (HBM) */
+    double atomic_latency_ns;      /* device-scope atomic round trip */
+    double launch_ns;              /* fixed cost of one kernel dispatch */
+} vx_hwinfo;
+
+/* One micro-kernel of the registry (a workgroup-level candidate). */
+typedef struct vx_kernel_info {
+    int id;
+    vx_dtype dtype;
+    int mb, nb, kb;                /* workgroup tile */
+    int wm, wn;                    /* wavefront grid; wavefront tile = (mb/wm) x (nb/wn) */
+    int mfma_m, mfma_n, mfma_k;    /* instruction tile */
+    int vec;                       /* 1: 16-byte vector loads (aligned operands only) */
+    int threads;
+    int lds_bytes;
+    int vgprs, agprs, sgprs;       /* from the compiler's resource report of this build */
+    int scratch_bytes;             /* per lane; 0 for every enabled kernel */
+    int enabled;
+} vx_kernel_info;
+
+/* A concrete execution plan for one call. */
+typedef struct vx_plan {
+    int kernel_id;
+    int split_k;                   /* K slices reduced in fp32 by the last-arriving workgroup */
+    int k_per_split;               /* K extent of one slice (a multiple of kb) */
+    int c_vec;                     /* 1: 4-element vector stores of C */
+    int64_t tiles_m, tiles_n;
+    int64_t grid;                  /* workgroups launched */
+    int group_m;
+    size_t workspace_bytes;        /* fp32 partials needed by split_k > 1 */
+    double predicted_ns;           /* the cost model's estimate for the call */
+    vx_kernel_info kernel;
+} vx_plan;
+
+/*
+ * C = A x B for one M x K by K x N product.
+ * M, N, K >= 0.  M == 0 or N == 0 is a no-op; K == 0 writes C := 0.
+ * A, B may be NULL only when their extent (M*K, K*N) is zero; C only when M*N is 0.
+ */
+vx_status vx_gemm(int64_t M, int64_t N, int64_t K, vx_dtype dtype,
+                  const void* A, const void* B, void* C, void* stream);
+
+/*
+ * Batched form: for b in [0, batch): C_b = A_b x B_b with
+ *   A_b = A + b*strideA, B_b = B + b*strideB, C_b = C + b*strideC   (strides in elements).
+ * strideB == 0 (or strideA == 0) broadcasts that operand to every batch.
+ * strideC must be >= M*N when batch > 1 (output batches may not overlap).
+ */
+vx_status vx_gemm_batched(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype,
+                          const void* A, int64_t strideA, const void* B, int64_t strideB,
+                          void* C, int64_t strideC, void* stream);
+
+/*
+ * The plan vx_gemm_batched would use, without launching anything (host only).
+ * base_align: the largest power of two dividing the byte addresses of A, B
+ * and C (0 means 256).  Strides as for vx_gemm_batched.
+ */
+vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype,
+                        int64_t strideA, int64_t strideB, int64_t strideC,
+                        uint64_t base_align, vx_plan* out);
+
+/*
+ * The cost model's estimate (ns) for running a given kernel with a given
+ * split-K factor on a shape; VX_ERR_NO_CANDIDATE if the pair is infeasible.
+ */
+vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype,
+                       int kernel_id, int split_k, int vec_ok, double* out_ns);
+
+/* Equation 2: T = t_load + (trips - 1) * max(t_load, cost_lower) + cost_lower + t_store
+ * (trips >= 1; trips == 0 gives t_store). */
+double vx_cost_temporal(double t_load, int64_t trips, double cost_lower, double t_store);
+/* Equation 3: ceil(parallel / units) for parallel >= 0, units >= 1 (else -1). */
+int64_t vx_cost_parallel_factor(int64_t parallel, int64_t units);
+
+/* Hardware description in use on the current device (or the override). */
+vx_status vx_get_hwinfo(vx_hwinfo* out);
+/* Replace the device description for planning (tests, what-if studies);
+ * NULL restores the real device.  Does not change which kernels exist. */
+vx_status vx_set_hwinfo_override(const vx_hwinfo* hw);
+
+/* Registry introspection. */
+int vx_registry_count(void);
+vx_status vx_registry_get(int id, vx_kernel_info* out);
+
+/*
+ * Pin every following call to one kernel and split-K factor (kernel_id < 0
+ * restores the analytical choice; split_k <= 0 lets the selector pick the
+ * split for the forced kernel).  For tests and ablation studies; process-wide.
+ * A forced kernel of the wrong dtype or alignment class makes calls return
+ * VX_ERR_NO_CANDIDATE.
+ */
+vx_status vx_force_plan(int kernel_id, int split_k);
+
+/*
+ * Hand the library a caller-owned device buffer to use as the split-K
+ * workspace of `stream` (NULL/0 bytes: return to the library's own lazily
+ * allocated buffer).  The buffer must stay valid until the stream's work
+ * using it has finished; the library zeroes its first 256 KiB (the arrival
+ * counters) with an asynchronous memset on `stream`.  bytes must be at least
+ * 256 KiB + the partials of the plans that will run.
+ */
+vx_status vx_set_workspace(void* ptr, size_t bytes, void* stream);
+
+const char* vx_status_string(vx_status s);
+const char* vx_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VX_H */

@@ -1,0 +1,442 @@
+// C ABI of the runtime-shaped GEMM library: argument checks, hardware
+// description, plan cache, split-K workspace, launch (Section 6.2: analytical
+// selection at run time, then the grid is computed from the runtime shape).
+#include <string.h>
+
+#include <atomic>
+#include <map>
+#include <mutex>
+#include <unordered_map>
+
+#include <hip/hip_runtime_api.h>
+
+#include "vx_internal.h"
+
+namespace {
+
+constexpr size_t kTicketBytes = 256 * 1024;                 // 65536 arrival counters
+constexpr size_t kDefaultPartials = 64ull * 1024 * 1024;   // fp32 split-K partials
+constexpr int kMaxDevices = 64;
+
+std::mutex g_mu;
+bool g_override_set = false;
+vx_hwinfo g_override;
+bool g_hw_valid[kMaxDevices];
+vx_hwinfo g_hw[kMaxDevices];
+std::atomic<int> g_force_id{-1};
+std::atomic<int> g_force_split{0};
+std::atomic<uint64_t> g_epoch{0};   // bumps when planning inputs change
+
+struct PlanKey {
+    int64_t batch, M, N, K;
+    int dt, vec_ok, c_vec, dev;
+    size_t ws;
+    uint64_t epoch;
+    bool operator==(const PlanKey& o) const
+    {
+        return batch == o.batch && M == o.M && N == o.N && K == o.K && dt == o.dt && vec_ok == o.vec_ok &&
+               c_vec == o.c_vec && dev == o.dev && ws == o.ws && epoch == o.epoch;
+    }
+};
+struct PlanKeyHash {
+    size_t operator()(const PlanKey& k) const
+    {
+        uint64_t h = 1469598103934665603ull;
+        auto mix = [&h](uint64_t v) { h = (h ^ v) * 1099511628211ull; };
+        mix(k.batch); mix(k.M); mix(k.N); mix(k.K);
+        mix(k.dt | (k.vec_ok << 4) | (k.c_vec << 5) | ((uint64_t)k.dev << 8));
+        mix(k.ws); mix(k.epoch);
+        return (size_t)h;
+    }
+};
+std::unordered_map<PlanKey, vx_plan, PlanKeyHash> g_plans;
+
+struct Workspace {
+    char* base = nullptr;
+    size_t bytes = 0;
+    bool owned = false;
+};
+std::map<std::pair<int, void*>, Workspace> g_ws;
+
+int elem_bytes(int dt) { return dt == VX_F32 ? 4 : 2; }
+
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes)
+{
+    if (!abytes || !bbytes)
+        return false;
+    uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+// Extent in elements of `batch` matrices of `elems` elements at `stride`.
+size_t extent(int64_t batch, int64_t stride, int64_t elems)
+{
+    if (batch <= 0 || elems <= 0)
+        return 0;
+    return (size_t)((batch - 1) * stride + elems);
+}
+
+vx_status hwinfo_for(int dev, vx_hwinfo* out)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_override_set) {
+        *out = g_override;
+        return VX_OK;
+    }
+    if (dev < 0 || dev >= kMaxDevices)
+        return VX_ERR_HIP;
+    if (!g_hw_valid[dev]) {
+        if (vxi_device_hwinfo(dev, &g_hw[dev]) != 0)
+            return VX_ERR_HIP;
+        g_hw_valid[dev] = true;
+    }
+    *out = g_hw[dev];
+    return VX_OK;
+}
+
+vx_status current_device(int* dev)
+{
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        if (g_override_set) {
+            *dev = -1;   // planning only; no device needed
+            return VX_OK;
+        }
+    }
+    if (hipGetDevice(dev) != hipSuccess)
+        return VX_ERR_HIP;
+    return VX_OK;
+}
+
+vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
+{
+    const int fid = g_force_id.load(), fsplit = g_force_split.load();
+    vx_hwinfo hw;
+    vx_status st = hwinfo_for(dev, &hw);
+    if (st != VX_OK)
+        return st;
+    VxLimits lim;
+    lim.ws_bytes = ws_bytes;
+    lim.max_tickets = ws_bytes ? (int64_t)(kTicketBytes / 4) : 0;
+    if (fid >= 0)
+        return vxi_select(hw, sh, lim, fid, fsplit, out);
+    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, g_epoch.load()};
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_plans.find(key);
+        if (it != g_plans.end()) {
+            *out = it->second;
+            return VX_OK;
+        }
+    }
+    st = vxi_select(hw, sh, lim, -1, 0, out);
+    if (st != VX_OK)
+        return st;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_plans.size() > (1u << 20))
+        g_plans.clear();
+    g_plans.emplace(key, *out);
+    return VX_OK;
+}
+
+// Workspace of (device, stream): returns its capacity for partials (0 if none yet).
+size_t ws_capacity(int dev, void* stream)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_ws.find({dev, stream});
+    if (it == g_ws.end())
+        return kDefaultPartials;   // will be allocated on first use
+    return it->second.bytes > kTicketBytes ? it->second.bytes - kTicketBytes : 0;
+}
+
+vx_status ws_get(int dev, void* stream, Workspace* out)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto key = std::make_pair(dev, stream);
+    auto it = g_ws.find(key);
+    if (it != g_ws.end()) {
+        *out = it->second;
+        return VX_OK;
+    }
+    Workspace w;
+    if (hipMalloc((void**)&w.base, kTicketBytes + kDefaultPartials) != hipSuccess) {
+        (void)hipGetLastError();
+        return VX_ERR_WORKSPACE;
+    }
+    w.bytes = kTicketBytes + kDefaultPartials;
+    w.owned = true;
+    if (hipMemsetAsync(w.base, 0, kTicketBytes, (hipStream_t)stream) != hipSuccess) {
+        (void)hipFree(w.base);
+        return VX_ERR_WORKSPACE;
+    }
+    g_ws[key] = w;
+    *out = w;
+    return VX_OK;
+}
+
+vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                    int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, void* stream)
+{
+    if (dtype != VX_F32 && dtype != VX_F16 && dtype != VX_BF16)
+        return VX_ERR_UNSUPPORTED_DTYPE;
+    if (batch < 0 || M < 0 || N < 0 || K < 0 || sA < 0 || sB < 0 || sC < 0)
+        return VX_ERR_INVALID_ARG;
+    if (M > INT32_MAX || N > INT32_MAX || K > INT32_MAX || batch > INT32_MAX)
+        return VX_ERR_INVALID_ARG;
+    const int eb = elem_bytes(dtype);
+    const size_t ea = extent(batch, sA, M * K), eb_ = extent(batch, sB, K * N), ec = extent(batch, sC, M * N);
+    if ((ea && !A) || (eb_ && !B) || (ec && !C))
+        return VX_ERR_INVALID_ARG;
+    if (batch > 1 && M * N > 0 && sC < M * N)
+        return VX_ERR_INVALID_ARG;
+    if (overlaps(C, ec * eb, A, ea * eb) || overlaps(C, ec * eb, B, eb_ * eb))
+        return VX_ERR_INVALID_ARG;
+    if (batch == 0 || M == 0 || N == 0)
+        return VX_OK;
+
+    VxShape sh;
+    sh.batch = batch;
+    sh.M = M;
+    sh.N = N;
+    sh.K = K;
+    sh.dt = dtype;
+    const int ve = 16 / eb;
+    const bool strides_vec = batch == 1 || ((sA % ve) == 0 && (sB % ve) == 0);
+    sh.vec_ok = (K % ve == 0) && (N % ve == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) &&
+                strides_vec;
+    sh.c_vec = (N % 4 == 0) && ((uintptr_t)C % (4 * eb) == 0) && (batch == 1 || sC % 4 == 0);
+
+    int dev = 0;
+    vx_status st = current_device(&dev);
+    if (st != VX_OK)
+        return st;
+    if (dev < 0)
+        return VX_ERR_HIP;   // planning override without a device: nothing to launch on
+
+    vx_plan plan;
+    st = plan_for(dev, sh, ws_capacity(dev, stream), &plan);
+    if (st != VX_OK)
+        return st;
+
+    Workspace ws;
+    if (plan.split_k > 1) {
+        if (ws_get(dev, stream, &ws) != VX_OK) {
+            st = plan_for(dev, sh, 0, &plan);   // fall back to plans without split-K
+            if (st != VX_OK)
+                return st;
+        }
+    }
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    if (plan.kernel_id < 0 || plan.kernel_id >= n)
+        return VX_ERR_NO_CANDIDATE;
+
+    vx_hwinfo hw;
+    st = hwinfo_for(dev, &hw);
+    if (st != VX_OK)
+        return st;
+
+    VxGemmArgs a;
+    a.A = A;
+    a.B = B;
+    a.C = C;
+    a.sA = sA;
+    a.sB = sB;
+    a.sC = sC;
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    a.tiles_m = (int)plan.tiles_m;
+    a.tiles_n = (int)plan.tiles_n;
+    a.split = plan.split_k;
+    a.k_per_split = plan.k_per_split;
+    a.batch = (int)batch;
+    a.group_m = plan.group_m;
+    a.num_xcd = hw.num_xcd;
+    a.c_vec = plan.c_vec;
+    a.ws = plan.split_k > 1 ? (float*)(ws.base + kTicketBytes) : nullptr;
+    a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
+    hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return VX_ERR_HIP;
+    }
+    return VX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+vx_status vx_gemm(int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A, const void* B, void* C,
+                  void* stream)
+{
+    return gemm_impl(1, M, N, K, dtype, A, M * K, B, K * N, C, M * N, stream);
+}
+
+vx_status vx_gemm_batched(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                          int64_t strideA, const void* B, int64_t strideB, void* C, int64_t strideC,
+                          void* stream)
+{
+    return gemm_impl(batch, M, N, K, dtype, A, strideA, B, strideB, C, strideC, stream);
+}
+
+vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, int64_t strideA,
+                        int64_t strideB, int64_t strideC, uint64_t base_align, vx_plan* out)
+{
+    if (dtype != VX_F32 && dtype != VX_F16 && dtype != VX_BF16)
+        return VX_ERR_UNSUPPORTED_DTYPE;
+    if (!out || batch < 1 || M < 1 || N < 1 || K < 0 || strideA < 0 || strideB < 0 || strideC < 0)
+        return VX_ERR_INVALID_ARG;
+    if (M > INT32_MAX || N > INT32_MAX || K > INT32_MAX || batch > INT32_MAX)
+        return VX_ERR_INVALID_ARG;
+    if (base_align == 0)
+        base_align = 256;
+    const int eb = elem_bytes(dtype), ve = 16 / eb;
+    VxShape sh;
+    sh.batch = batch;
+    sh.M = M;
+    sh.N = N;
+    sh.K = K;
+    sh.dt = dtype;
+    const bool strides_vec = batch == 1 || ((strideA % ve) == 0 && (strideB % ve) == 0);
+    sh.vec_ok = (K % ve == 0) && (N % ve == 0) && (base_align % 16 == 0) && strides_vec;
+    sh.c_vec = (N % 4 == 0) && (base_align % (4 * eb) == 0) && (batch == 1 || strideC % 4 == 0);
+    int dev = 0;
+    vx_status st = current_device(&dev);
+    if (st != VX_OK)
+        return st;
+    return plan_for(dev, sh, dev < 0 ? kDefaultPartials : ws_capacity(dev, nullptr), out);
+}
+
+vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, int kernel_id,
+                       int split_k, int vec_ok, double* out_ns)
+{
+    if (dtype != VX_F32 && dtype != VX_F16 && dtype != VX_BF16)
+        return VX_ERR_UNSUPPORTED_DTYPE;
+    if (!out_ns || batch < 1 || M < 1 || N < 1 || K < 0)
+        return VX_ERR_INVALID_ARG;
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    if (kernel_id < 0 || kernel_id >= n)
+        return VX_ERR_NO_CANDIDATE;
+    int dev = 0;
+    vx_status st = current_device(&dev);
+    if (st != VX_OK)
+        return st;
+    vx_hwinfo hw;
+    st = hwinfo_for(dev, &hw);
+    if (st != VX_OK)
+        return st;
+    VxShape sh{batch, M, N, K, (int)dtype, vec_ok ? 1 : 0, 1};
+    VxLimits lim{kDefaultPartials, (int64_t)(kTicketBytes / 4)};
+    const double c = vxi_cost(hw, sh, reg[kernel_id].info, split_k, lim, nullptr);
+    if (c < 0.0)
+        return VX_ERR_NO_CANDIDATE;
+    *out_ns = c;
+    return VX_OK;
+}
+
+vx_status vx_get_hwinfo(vx_hwinfo* out)
+{
+    if (!out)
+        return VX_ERR_INVALID_ARG;
+    int dev = 0;
+    vx_status st = current_device(&dev);
+    if (st != VX_OK)
+        return st;
+    return hwinfo_for(dev, out);
+}
+
+vx_status vx_set_hwinfo_override(const vx_hwinfo* hw)
+{
+    if (hw && (hw->num_cu < 1 || hw->simd_per_cu < 1 || hw->lds_bytes_per_cu < 1 || hw->clock_ghz <= 0.0 ||
+               hw->hbm_gbps <= 0.0 || hw->vgprs_per_lane < 1 || hw->max_waves_per_simd < 1 ||
+               hw->mfma_flop_clk_cu_f16 <= 0.0 || hw->mfma_flop_clk_cu_f32 <= 0.0 ||
+               hw->l2_bytes_clk_cu <= 0.0 || hw->lds_bytes_clk_cu <= 0.0 || hw->num_xcd < 1))
+        return VX_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_override_set = hw != nullptr;
+    if (hw)
+        g_override = *hw;
+    g_plans.clear();
+    g_epoch.fetch_add(1);
+    return VX_OK;
+}
+
+int vx_registry_count(void)
+{
+    int n = 0;
+    vxi_registry(&n);
+    return n;
+}
+
+vx_status vx_registry_get(int id, vx_kernel_info* out)
+{
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    if (!out || id < 0 || id >= n)
+        return VX_ERR_INVALID_ARG;
+    *out = reg[id].info;
+    return VX_OK;
+}
+
+vx_status vx_force_plan(int kernel_id, int split_k)
+{
+    if (kernel_id >= vx_registry_count())
+        return VX_ERR_NO_CANDIDATE;
+    g_force_id.store(kernel_id < 0 ? -1 : kernel_id);
+    g_force_split.store(split_k > 0 ? split_k : 0);
+    return VX_OK;
+}
+
+vx_status vx_set_workspace(void* ptr, size_t bytes, void* stream)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return VX_ERR_HIP;
+    if (ptr && bytes < kTicketBytes)
+        return VX_ERR_INVALID_ARG;
+    if ((uintptr_t)ptr % 256)
+        return VX_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto key = std::make_pair(dev, stream);
+    auto it = g_ws.find(key);
+    if (it != g_ws.end()) {
+        if (it->second.owned) {
+            // the stream may still be using it: free after the stream's work
+            if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
+                return VX_ERR_HIP;
+            (void)hipFree(it->second.base);
+        }
+        g_ws.erase(it);
+    }
+    if (ptr) {
+        if (hipMemsetAsync(ptr, 0, kTicketBytes, (hipStream_t)stream) != hipSuccess)
+            return VX_ERR_HIP;
+        Workspace w;
+        w.base = (char*)ptr;
+        w.bytes = bytes;
+        w.owned = false;
+        g_ws[key] = w;
+    }
+    g_epoch.fetch_add(1);
+    return VX_OK;
+}
+
+const char* vx_status_string(vx_status s)
+{
+    switch (s) {
+    case VX_OK: return "VX_OK";
+    case VX_ERR_INVALID_ARG: return "VX_ERR_INVALID_ARG";
+    case VX_ERR_UNSUPPORTED_DTYPE: return "VX_ERR_UNSUPPORTED_DTYPE";
+    case VX_ERR_NO_CANDIDATE: return "VX_ERR_NO_CANDIDATE";
+    case VX_ERR_WORKSPACE: return "VX_ERR_WORKSPACE";
+    case VX_ERR_HIP: return "VX_ERR_HIP";
+    }
+    return "VX_ERR_UNKNOWN";
+}
+
+const char* vx_version(void) { return "vx 0.1 (gfx950)"; }
+
+}  // extern "C"

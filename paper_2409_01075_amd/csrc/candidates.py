@@ -1,0 +1,204 @@
+"""Build-time candidate generation (Section 5.1, Algorithm 2) for gfx950.
+
+Runs once, offline, when the library is built: it derives the micro-kernel
+candidates of every level bottom-up from the hardware description, keeping at
+each level only tiles that are integer multiples of a candidate of the level
+below, and records the upper -> lower links.  The surviving workgroup-level
+candidates become the kernel instantiations compiled into the library; the
+runtime selector then chooses among them analytically (Section 5.2).
+
+Levels (Table 1, GPU rows):
+  L0  MFMA instruction tile (m0, n0, k0): filtered by the ISA (FilterByISA).
+  L1  wavefront tile (Mw, Nw): register level, multiples of an L0 tile.
+  L2  workgroup tile (Mb, Nb, Kb) with wm x wn wavefronts: LDS level,
+      multiples of an L1 tile (FilterByMultiples).
+The grid level has no tile of its own: it is the runtime parallel loop.
+
+Feasible range (the paper prunes candidates whose use of a hardware level is
+"extremely low or high" without giving thresholds; the thresholds below are
+this library's reading):
+  * L1: accumulator registers Mw*Nw/64 in [4, 128] of the 512 per lane, so
+    staging, fragments and addresses fit without spilling; aspect <= 4.
+  * L2: 4 wavefronts per workgroup (one per SIMD of the CU), or 8 for tiles of
+    at least 128 x 128; LDS for a 2-stage ring <= 160 KiB; every thread moves
+    at least one 16-byte vector of A and of B per K step and at most 32 (<= 128
+    staging VGPRs); the K step reads at least 128 contiguous bytes per row (two
+    64-byte segments); aspect of the workgroup tile <= 8.
+  * L0 per L1 link: the 32 x 32 MFMA when both wavefront dims are multiples of
+    32 and at least 64 (half the fragment loads per FLOP of the 16 x 16 shape),
+    else the 16 x 16 MFMA.  The paper takes this decision by profiling L0
+    offline; until such a calibration exists this fixed rule stands in.
+"""
+import itertools
+import json
+import sys
+
+GFX950 = {
+    "arch": "gfx950",
+    "lds_bytes": 160 * 1024,
+    "vgprs_per_lane": 512,
+    "max_threads": 1024,
+    "wave": 64,
+    # MFMA instructions with fp32 accumulation: (m, n, k) per dtype
+    "mfma": {
+        "f16": [(16, 16, 32), (32, 32, 16)],
+        "bf16": [(16, 16, 32), (32, 32, 16)],
+        "f32": [(16, 16, 4), (32, 32, 2)],
+    },
+}
+DT_CODE = {"f32": 0, "f16": 1, "bf16": 2}
+ELEM_BYTES = {"f32": 4, "f16": 2, "bf16": 2}
+
+
+def get_hardware_info(level, hw=GFX950):
+    return hw
+
+
+# ------------------------------------------------------------------ L0 -----
+def init_cands_l0(hw):
+    dims = [4, 8, 16, 32, 64]
+    ks = [1, 2, 4, 8, 16, 32, 64]
+    return [(m, n, k) for m in dims for n in dims for k in ks]
+
+
+def filter_by_isa(cands, dtype, hw):
+    legal = set(hw["mfma"][dtype])
+    return [c for c in cands if c in legal]
+
+
+# ------------------------------------------------------------------ L1 -----
+def init_cands_l1(hw):
+    out = []
+    for mw in (16, 32, 64, 128, 256):
+        for nw in (16, 32, 64, 128, 256):
+            acc = mw * nw // hw["wave"]
+            if 4 <= acc <= 128 and max(mw, nw) <= 4 * min(mw, nw):
+                out.append((mw, nw))
+    return out
+
+
+def multiples_l1(prev, cands):
+    m0, n0, _ = prev
+    return [c for c in cands if c[0] % m0 == 0 and c[1] % n0 == 0]
+
+
+# ------------------------------------------------------------------ L2 -----
+WAVE_GRIDS = [(1, 1), (1, 2), (2, 1), (2, 2), (1, 4), (4, 1), (2, 4), (4, 2)]
+
+
+def lds_bytes(dtype, mb, nb, kb):
+    eb = ELEM_BYTES[dtype]
+    pad = 16 // eb
+    if eb == 2:
+        stage = (mb * (kb + pad) + nb * (kb + pad)) * eb
+    else:
+        stage = (mb * (kb + pad) + kb * (nb + 4)) * eb
+    return 2 * stage
+
+
+def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw):
+    eb = ELEM_BYTES[dtype]
+    nt = wm * wn * hw["wave"]
+    ve = 16 // eb
+    if nt > hw["max_threads"]:
+        return False
+    waves = wm * wn
+    if waves != 4 and not (waves == 8 and mb >= 128 and nb >= 128):
+        return False
+    if max(mb, nb) > 8 * min(mb, nb) or max(mb, nb) > 256:
+        return False
+    if kb * eb < 128:
+        return False
+    if lds_bytes(dtype, mb, nb, kb) > hw["lds_bytes"]:
+        return False
+    a_vec = mb * kb // ve
+    b_vec = nb * kb // ve
+    if a_vec % nt or b_vec % nt:
+        return False
+    if not (1 <= a_vec // nt <= 32 and 1 <= b_vec // nt <= 32):
+        return False
+    if a_vec // nt + b_vec // nt > 32:
+        return False
+    # K chunk of one fragment load
+    kch = (32 if mi == 16 else 16) if eb == 2 else (16 if mi == 16 else 8)
+    if kb % kch:
+        return False
+    if eb == 2:
+        # B is staged in blocks of BK rows x 8 columns (BK in {8, 4, 2})
+        ok = False
+        for bk in (8, 4, 2):
+            blocks = (kb // bk) * (nb // 8)
+            if blocks >= nt and blocks % nt == 0:
+                ok = True
+                break
+        if not ok:
+            return False
+    return True
+
+
+def generate_candidates_for_layer(level, dtype, hw=GFX950):
+    """Algorithm 2: returns (cands, link) for `level`; link maps a candidate
+    to the list of lower-level candidates it is an integer multiple of."""
+    hw = get_hardware_info(level, hw)
+    if level == 0:
+        return filter_by_isa(init_cands_l0(hw), dtype, hw), {}
+    prev, _ = generate_candidates_for_layer(level - 1, dtype, hw)
+    cands, link = [], {}
+    if level == 1:
+        init = init_cands_l1(hw)
+        for p in prev:
+            for c in multiples_l1(p, init):
+                if c not in link:
+                    cands.append(c)
+                    link[c] = []
+                link[c].append(p)
+        return cands, link
+    if level == 2:
+        l1_links = generate_candidates_for_layer(1, dtype, hw)[1]
+        kbs = (64, 128, 256) if ELEM_BYTES[dtype] == 2 else (32, 64)
+        for (mw, nw) in prev:
+            for (wm, wn) in WAVE_GRIDS:
+                for kb in kbs:
+                    for l0 in l1_links[(mw, nw)]:
+                        mi = l0[0]
+                        want = 32 if (mw % 32 == 0 and nw % 32 == 0 and min(mw, nw) >= 64) else 16
+                        if mi != want or kb % l0[2]:
+                            continue
+                        c = (wm * mw, wn * nw, kb, wm, wn, mi)
+                        if not feasible_l2(dtype, *c, hw):
+                            continue
+                        if c not in link:
+                            cands.append(c)
+                            link[c] = []
+                        link[c].append(((mw, nw), l0))
+        return cands, link
+    raise ValueError("gfx950 GEMM has levels 0..2")
+
+
+def registry(hw=GFX950):
+    """All workgroup-level candidates of every dtype, with the load variant.
+
+    Each candidate is compiled twice: with 16-byte vector loads (operands whose
+    row strides and base addresses are 16-byte aligned) and with element-wise
+    loads (any alignment)."""
+    out = []
+    for dtype in ("f16", "bf16", "f32"):
+        cands, link = generate_candidates_for_layer(2, dtype, hw)
+        for (mb, nb, kb, wm, wn, mi) in cands:
+            for vec in (1, 0):
+                out.append(dict(dtype=dtype, dt=DT_CODE[dtype], mb=mb, nb=nb, kb=kb, wm=wm, wn=wn,
+                                mi=mi, vec=vec, threads=wm * wn * hw["wave"],
+                                lds=lds_bytes(dtype, mb, nb, kb)))
+    for i, e in enumerate(out):
+        e["id"] = i
+    return out
+
+
+if __name__ == "__main__":
+    reg = registry()
+    for dt in ("f16", "bf16", "f32"):
+        for lv in (0, 1, 2):
+            c, _ = generate_candidates_for_layer(lv, dt)
+            print(dt, "L%d" % lv, len(c), file=sys.stderr)
+    print(len(reg), file=sys.stderr)
+    json.dump(reg, sys.stdout, indent=0)

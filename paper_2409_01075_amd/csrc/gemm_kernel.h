@@ -1,0 +1,508 @@
+// Runtime-shaped dense GEMM C = A x B for gfx950 (CDNA4), row-major, fp32
+// accumulation.  One template covers every registry candidate.
+//
+// The hierarchy follows the unified recursive abstraction (Section 4.2,
+// Algorithm 1, with the GPU rows of Table 1):
+//   level 2  grid       parallel loops over (batch, K slice, tile): no load/store
+//   level 1  workgroup  temporal reduction loop over K in Kb steps; each step
+//                       loads the A and B tiles from global memory into a
+//                       2-stage LDS ring (prefetch of step k+1 overlaps the
+//                       MFMAs of step k), then runs level 0
+//   level 0  wavefront  LDS -> VGPR fragment loads and MFMA instructions, with
+//                       the fp32 accumulators kept in registers until Store
+// Every level's tile is an integer multiple of the level below (Section 5.1);
+// partial tiles at the M, N and K edges are predicated, never padded.
+//
+// Operand order: the MFMA is issued as D = Bt * At, i.e. with the B fragment
+// in the instruction's A slot and the A fragment in its B slot.  Each lane
+// then owns 4 consecutive output columns of one C row, so the epilogue writes
+// row-major C with 4-element vector stores.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "vx_args.h"
+
+namespace vxk {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+enum { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
+
+// Compile-time description of one candidate: workgroup tile Mb x Nb x Kb,
+// WM x WN wavefronts, MFMA instruction tile MI x MI, vector (16-byte) or
+// element-wise global loads.
+template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, bool VEC_>
+struct Cfg {
+    static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_;
+    static constexpr bool VEC = VEC_;
+    static constexpr bool H = DT != DT_F32;              // 16-bit inputs
+    static constexpr int NT = WM * WN * 64;              // threads per workgroup
+    static constexpr int MW = MB / WM, NW = NB / WN;     // wavefront tile
+    static constexpr int FM = MW / MI, FN = NW / MI;     // MFMA tiles per wavefront
+    static constexpr int ACC = MI == 16 ? 4 : 16;        // fp32 accumulators per lane per MFMA tile
+    static constexpr int EB = H ? 2 : 4;                 // bytes per element
+    static constexpr int VE = 16 / EB;                   // elements per 16-byte vector
+    static constexpr int PADK = 16 / EB;                 // LDS row padding, elements
+    static constexpr int LDA = KB + PADK;                // As[m][k]
+    static constexpr int LDB = H ? KB + PADK : NB + 4;   // 16-bit: Bs[n][k]; fp32: Bs[k][n]
+    static constexpr int A_ELEMS = MB * LDA;
+    static constexpr int B_ELEMS = H ? NB * LDB : KB * LDB;
+    static constexpr int STAGE_BYTES = (A_ELEMS + B_ELEMS) * EB;
+    static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+    // A tile: MB*KB/VE vectors along k
+    static constexpr int AV = MB * KB / VE / NT;
+    // B tile, 16-bit: blocks of BK k-rows x 8 columns, transposed on the way into LDS
+    static constexpr int BK = !H ? 1 : ((KB / 8) * (NB / 8) % NT == 0 && (KB / 8) * (NB / 8) >= NT) ? 8
+                                     : ((KB / 4) * (NB / 8) % NT == 0 && (KB / 4) * (NB / 8) >= NT) ? 4 : 2;
+    static constexpr int KBB = KB / BK;                  // k-blocks per tile
+    static constexpr int BBLK = H ? KBB * (NB / 8) / NT : 0;
+    // B tile, fp32: KB*NB/4 vectors along n; 16-bit element-wise path: NB*KB/8 k-vectors
+    static constexpr int BV = H ? NB * KB / 8 / NT : KB * NB / 4 / NT;
+    static constexpr int KI = H ? (MI == 16 ? 32 : 16) : (MI == 16 ? 4 : 2);   // K per MFMA
+    static constexpr int KCH = H ? KI : (MI == 16 ? 16 : 8);                      // K per fragment load
+
+    static_assert(MB % WM == 0 && NB % WN == 0, "waves must tile the workgroup tile");
+    static_assert(MW % MI == 0 && NW % MI == 0, "MFMA tiles must tile the wavefront tile");
+    static_assert(KB % KCH == 0, "Kb must be a multiple of the MFMA K chunk");
+    static_assert(AV >= 1 && AV * VE * NT == MB * KB, "A tile must split evenly over threads");
+    static_assert(BV >= 1 && (H ? BV * 8 : BV * 4) * NT == NB * KB, "B tile must split evenly over threads");
+    static_assert(!H || !VEC || (BBLK >= 1 && BBLK * NT * BK * 8 == KB * NB), "B blocks must split evenly");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one CU");
+};
+
+__device__ __forceinline__ unsigned lo16(unsigned w) { return w & 0xffffu; }
+__device__ __forceinline__ unsigned hi16(unsigned w) { return w >> 16; }
+__device__ __forceinline__ unsigned pack2(unsigned lo, unsigned hi) { return (lo & 0xffffu) | (hi << 16); }
+// element j (0..7) of a vector of eight 16-bit values
+__device__ __forceinline__ unsigned elem16(const u32x4& v, int j)
+{
+    unsigned w = v[j >> 1];
+    return (j & 1) ? hi16(w) : lo16(w);
+}
+
+template <class C>
+struct Tile {
+    // ---------------------------------------------------------- Load (level 1)
+    // Registers holding one K step of A and B between the global load and the
+    // LDS store.
+    u32x4 ra[C::AV];
+    u32x4 rb[C::H && C::VEC ? C::BBLK * C::BK : C::BV];
+
+    // Global -> registers for the K step starting at k0 (< kend).
+    __device__ __forceinline__ void load(const char* __restrict__ Ab, const char* __restrict__ Bb,
+                                         int m0, int n0, int k0, int kend, int M, int N, int K, int t)
+    {
+        // A: MB x KB, 16-byte vectors along k
+#pragma unroll
+        for (int v = 0; v < C::AV; ++v) {
+            const int idx = t + v * C::NT;
+            const int r = idx / (C::KB / C::VE), c = idx % (C::KB / C::VE);
+            const int gm = m0 + r, gk = k0 + c * C::VE;
+            const char* p = Ab + ((int64_t)gm * K + gk) * C::EB;
+            if (C::VEC) {
+                ra[v] = (gm < M && gk < kend) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
+            } else {
+                u32x4 x = {0, 0, 0, 0};
+                if (gm < M) {
+                    if (C::H) {
+#pragma unroll
+                        for (int e = 0; e < 8; e += 2) {
+                            unsigned lo = gk + e < kend ? ((const uint16_t*)p)[e] : 0u;
+                            unsigned hi = gk + e + 1 < kend ? ((const uint16_t*)p)[e + 1] : 0u;
+                            x[e >> 1] = pack2(lo, hi);
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            x[e] = gk + e < kend ? ((const unsigned*)p)[e] : 0u;
+                    }
+                }
+                ra[v] = x;
+            }
+        }
+        if (C::H && C::VEC) {
+            // B: blocks of BK rows x 8 columns (16 bytes per row)
+#pragma unroll
+            for (int i = 0; i < C::BBLK; ++i) {
+                const int idx = t + i * C::NT;
+                const int kb = idx % C::KBB, nb = idx / C::KBB;
+                const int gn = n0 + nb * 8;
+#pragma unroll
+                for (int r = 0; r < C::BK; ++r) {
+                    const int gk = k0 + kb * C::BK + r;
+                    const char* p = Bb + ((int64_t)gk * N + gn) * 2;
+                    rb[i * C::BK + r] = (gk < kend && gn < N) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
+                }
+            }
+        } else if (C::H) {
+            // B, element-wise: each thread gathers 8 consecutive k of one column
+#pragma unroll
+            for (int v = 0; v < C::BV; ++v) {
+                const int idx = t + v * C::NT;
+                const int n = idx % C::NB, kv = idx / C::NB;
+                const int gn = n0 + n, gk = k0 + kv * 8;
+                const uint16_t* p = (const uint16_t*)Bb + (int64_t)gk * N + gn;
+                u32x4 x = {0, 0, 0, 0};
+                if (gn < N) {
+#pragma unroll
+                    for (int e = 0; e < 8; e += 2) {
+                        unsigned lo = gk + e < kend ? p[(int64_t)e * N] : 0u;
+                        unsigned hi = gk + e + 1 < kend ? p[(int64_t)(e + 1) * N] : 0u;
+                        x[e >> 1] = pack2(lo, hi);
+                    }
+                }
+                rb[v] = x;
+            }
+        } else {
+            // fp32 B: natural layout, 4 consecutive columns per vector
+#pragma unroll
+            for (int v = 0; v < C::BV; ++v) {
+                const int idx = t + v * C::NT;
+                const int c = idx % (C::NB / 4), kr = idx / (C::NB / 4);
+                const int gn = n0 + c * 4, gk = k0 + kr;
+                const char* p = Bb + ((int64_t)gk * N + gn) * 4;
+                if (C::VEC) {
+                    rb[v] = (gk < kend && gn < N) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
+                } else {
+                    u32x4 x = {0, 0, 0, 0};
+                    if (gk < kend) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            x[e] = gn + e < N ? ((const unsigned*)p)[e] : 0u;
+                    }
+                    rb[v] = x;
+                }
+            }
+        }
+    }
+
+    // Registers -> LDS stage.
+    __device__ __forceinline__ void store(char* __restrict__ stage, int t)
+    {
+        char* As = stage;
+        char* Bs = stage + C::A_ELEMS * C::EB;
+#pragma unroll
+        for (int v = 0; v < C::AV; ++v) {
+            const int idx = t + v * C::NT;
+            const int r = idx / (C::KB / C::VE), c = idx % (C::KB / C::VE);
+            *(u32x4*)(As + (r * C::LDA + c * C::VE) * C::EB) = ra[v];
+        }
+        if (C::H && C::VEC) {
+            // transpose each BK x 8 block into 8 k-vectors (one per column)
+#pragma unroll
+            for (int i = 0; i < C::BBLK; ++i) {
+                const int idx = t + i * C::NT;
+                const int kb = idx % C::KBB, nb = idx / C::KBB;
+                const u32x4* in = &rb[i * C::BK];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    char* dst = Bs + ((nb * 8 + j) * C::LDB + kb * C::BK) * 2;
+                    if (C::BK == 8) {
+                        u32x4 o;
+#pragma unroll
+                        for (int d = 0; d < 4; ++d)
+                            o[d] = pack2(elem16(in[2 * d], j), elem16(in[2 * d + 1], j));
+                        *(u32x4*)dst = o;
+                    } else if (C::BK == 4) {
+                        u32x2 o;
+#pragma unroll
+                        for (int d = 0; d < 2; ++d)
+                            o[d] = pack2(elem16(in[2 * d], j), elem16(in[2 * d + 1], j));
+                        *(u32x2*)dst = o;
+                    } else {
+                        *(unsigned*)dst = pack2(elem16(in[0], j), elem16(in[1], j));
+                    }
+                }
+            }
+        } else if (C::H) {
+#pragma unroll
+            for (int v = 0; v < C::BV; ++v) {
+                const int idx = t + v * C::NT;
+                const int n = idx % C::NB, kv = idx / C::NB;
+                *(u32x4*)(Bs + (n * C::LDB + kv * 8) * 2) = rb[v];
+            }
+        } else {
+#pragma unroll
+            for (int v = 0; v < C::BV; ++v) {
+                const int idx = t + v * C::NT;
+                const int c = idx % (C::NB / 4), kr = idx / (C::NB / 4);
+                *(u32x4*)(Bs + (kr * C::LDB + c * 4) * 4) = rb[v];
+            }
+        }
+    }
+};
+
+// ------------------------------------------------------------- level 0 -----
+template <int DT, int MI>
+__device__ __forceinline__ void mfma16(const u32x4& a, const u32x4& b, f32x4& acc)
+{
+    if (DT == DT_F16)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
+    else
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+}
+template <int DT>
+__device__ __forceinline__ void mfma32(const u32x4& a, const u32x4& b, f32x16& acc)
+{
+    if (DT == DT_F16)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
+    else
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+}
+
+template <class C>
+struct Acc {
+    typedef typename std::conditional<C::MI == 16, f32x4, f32x16>::type T;
+    T v[C::FN][C::FM];
+};
+
+// One K step of the wavefront tile out of LDS stage `stage`.
+template <class C>
+__device__ __forceinline__ void compute_step(const char* __restrict__ stage, Acc<C>& acc, int wm0, int wn0, int lane)
+{
+    const char* As = stage;
+    const char* Bs = stage + C::A_ELEMS * C::EB;
+    const int li = lane % C::MI, lg = lane / C::MI;
+    if (C::H) {
+#pragma unroll
+        for (int kk = 0; kk < C::KB / C::KI; ++kk) {
+            u32x4 fa[C::FM], fb[C::FN];
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm)
+                fa[fm] = *(const u32x4*)(As + ((wm0 + fm * C::MI + li) * C::LDA + kk * C::KI + lg * 8) * 2);
+#pragma unroll
+            for (int fn = 0; fn < C::FN; ++fn)
+                fb[fn] = *(const u32x4*)(Bs + ((wn0 + fn * C::MI + li) * C::LDB + kk * C::KI + lg * 8) * 2);
+#pragma unroll
+            for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+                for (int fm = 0; fm < C::FM; ++fm) {
+                    if constexpr (C::MI == 16)
+                        mfma16<C::DT, 16>(fb[fn], fa[fm], acc.v[fn][fm]);
+                    else
+                        mfma32<C::DT>(fb[fn], fa[fm], acc.v[fn][fm]);
+                }
+        }
+    } else {
+        // fp32: a lane's 4 k values per fragment are k = chunk + 4*lg + s (s = 0..3);
+        // any k order is valid as long as both operands use the same one.
+#pragma unroll
+        for (int kc = 0; kc < C::KB / C::KCH; ++kc) {
+            f32x4 fa[C::FM];
+            float fb[C::FN][4];
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm)
+                fa[fm] = *(const f32x4*)(As + ((wm0 + fm * C::MI + li) * C::LDA + kc * C::KCH + lg * 4) * 4);
+#pragma unroll
+            for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    fb[fn][s] = *(const float*)(Bs + ((kc * C::KCH + lg * 4 + s) * C::LDB + wn0 + fn * C::MI + li) * 4);
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+                    for (int fm = 0; fm < C::FM; ++fm) {
+                        if constexpr (C::MI == 16)
+                            acc.v[fn][fm] = __builtin_amdgcn_mfma_f32_16x16x4f32(fb[fn][s], fa[fm][s], acc.v[fn][fm], 0, 0, 0);
+                        else
+                            acc.v[fn][fm] = __builtin_amdgcn_mfma_f32_32x32x2f32(fb[fn][s], fa[fm][s], acc.v[fn][fm], 0, 0, 0);
+                    }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- Store ----
+template <int DT>
+__device__ __forceinline__ void store4(char* __restrict__ Cb, int64_t off, int n, int N, bool vec, float a0, float a1, float a2, float a3)
+{
+    if (DT == DT_F32) {
+        float* p = (float*)Cb + off;
+        if (vec && n + 3 < N) {
+            *(f32x4*)p = f32x4{a0, a1, a2, a3};
+        } else {
+            if (n < N) p[0] = a0;
+            if (n + 1 < N) p[1] = a1;
+            if (n + 2 < N) p[2] = a2;
+            if (n + 3 < N) p[3] = a3;
+        }
+    } else {
+        uint16_t h[4];
+        if (DT == DT_F16) {
+            h[0] = __builtin_bit_cast(uint16_t, (_Float16)a0);
+            h[1] = __builtin_bit_cast(uint16_t, (_Float16)a1);
+            h[2] = __builtin_bit_cast(uint16_t, (_Float16)a2);
+            h[3] = __builtin_bit_cast(uint16_t, (_Float16)a3);
+        } else {
+            h[0] = __builtin_bit_cast(uint16_t, (__bf16)a0);
+            h[1] = __builtin_bit_cast(uint16_t, (__bf16)a1);
+            h[2] = __builtin_bit_cast(uint16_t, (__bf16)a2);
+            h[3] = __builtin_bit_cast(uint16_t, (__bf16)a3);
+        }
+        uint16_t* p = (uint16_t*)Cb + off;
+        if (vec && n + 3 < N) {
+            *(u32x2*)p = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+        } else {
+            if (n < N) p[0] = h[0];
+            if (n + 1 < N) p[1] = h[1];
+            if (n + 2 < N) p[2] = h[2];
+            if (n + 3 < N) p[3] = h[3];
+        }
+    }
+}
+
+// Lane -> C coordinates of accumulator group g (4 consecutive columns) of one
+// MFMA tile, relative to the tile's corner (operands issued as Bt * At).
+template <int MI>
+__device__ __forceinline__ void acc_coord(int lane, int g, int& dm, int& dn)
+{
+    if (MI == 16) {
+        dm = lane % 16;
+        dn = 4 * (lane / 16);
+    } else {
+        dm = lane % 32;
+        dn = 8 * g + 4 * (lane / 32);
+    }
+}
+
+// ------------------------------------------------------- level 2 + level 1 --
+template <class C>
+__device__ __forceinline__ void gemm_body(const VxGemmArgs& p)
+{
+    __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
+
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+
+    // Grid level: workgroups are dispatched round-robin over the XCDs; remap
+    // the linear id so that each XCD receives a contiguous range of logical
+    // tiles (neighbouring tiles share A or B panels in that XCD's L2).
+    const int G = gridDim.x, w = blockIdx.x;
+    const int nx = p.num_xcd;
+    const int xcd = w % nx, q = G / nx, rem = G % nx;
+    const int wl = xcd * q + (xcd < rem ? xcd : rem) + w / nx;
+
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int tile = wl % tiles;
+    const int bz = wl / tiles;
+    const int z = bz % p.split, b = bz / p.split;
+    // grouped order: group_m tile rows are walked column by column
+    const int per_group = p.group_m * p.tiles_n;
+    const int grp = tile / per_group;
+    const int first_m = grp * p.group_m;
+    const int gm = min(p.group_m, p.tiles_m - first_m);
+    const int tm = first_m + (tile % per_group) % gm;
+    const int tn = (tile % per_group) / gm;
+
+    const int m0 = tm * C::MB, n0 = tn * C::NB;
+    const int kbeg = z * p.k_per_split;
+    const int kend = min(p.K, kbeg + p.k_per_split);
+    const int nk = kend > kbeg ? (kend - kbeg + C::KB - 1) / C::KB : 0;
+
+    const char* Ab = (const char*)p.A + ((int64_t)b * p.sA + (int64_t)m0 * p.K) * C::EB;
+    const char* Bb = (const char*)p.B + (int64_t)b * p.sB * C::EB;
+    const int Mrel = p.M - m0;
+
+    const int wm0 = (wave % C::WM) * C::MW, wn0 = (wave / C::WM) * C::NW;
+
+    Acc<C> acc;
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+            for (int e = 0; e < C::ACC; ++e)
+                acc.v[fn][fm][e] = 0.0f;
+
+    Tile<C> tl;
+    if (nk > 0) {
+        tl.load(Ab, Bb, 0, n0, kbeg, kend, Mrel, p.N, p.K, t);
+        tl.store(smem, t);
+    }
+    __syncthreads();
+    for (int it = 0; it < nk; ++it) {
+        char* cur = smem + (it & 1) * C::STAGE_BYTES;
+        if (it + 1 < nk)
+            tl.load(Ab, Bb, 0, n0, kbeg + (it + 1) * C::KB, kend, Mrel, p.N, p.K, t);
+        compute_step<C>(cur, acc, wm0, wn0, lane);
+        if (it + 1 < nk)
+            tl.store(smem + ((it + 1) & 1) * C::STAGE_BYTES, t);
+        __syncthreads();
+    }
+
+    char* Cb = (char*)p.C + (int64_t)b * p.sC * C::EB;
+    constexpr int NG = C::ACC / 4;
+
+    if (p.split > 1) {
+        // Split-K: publish this slice's fp32 partial tile, then the last slice
+        // to arrive sums all slices in order 0..split-1 and writes C.
+        // The partials travel through device-coherent (agent-scope) stores and
+        // loads, so no workgroup has to write back or invalidate a whole L2.
+        constexpr int PER = C::FN * C::FM * C::ACC;       // floats per thread
+        const int64_t tile_id = (int64_t)b * tiles + tm * p.tiles_n + tn;
+        float* wt = p.ws + tile_id * (int64_t)p.split * (PER * C::NT);
+        float* mine = wt + (int64_t)z * (PER * C::NT);
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+                for (int e = 0; e < C::ACC; ++e)
+                    __hip_atomic_store(&mine[((fn * C::FM + fm) * C::ACC + e) * C::NT + t], acc.v[fn][fm][e],
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // every store of the partial tile has completed before the arrival is counted
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        __shared__ unsigned arrived;
+        if (t == 0)
+            arrived = __hip_atomic_fetch_add(&p.tickets[tile_id], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        if (arrived != (unsigned)(p.split - 1))
+            return;
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+                for (int e = 0; e < C::ACC; ++e) {
+                    const int64_t o = ((fn * C::FM + fm) * C::ACC + e) * C::NT + t;
+                    float s = z == 0 ? acc.v[fn][fm][e]
+                                     : __hip_atomic_load(wt + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    for (int zz = 1; zz < p.split; ++zz)
+                        s += zz == z ? acc.v[fn][fm][e]
+                                     : __hip_atomic_load(wt + (int64_t)zz * (PER * C::NT) + o, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+                    acc.v[fn][fm][e] = s;
+                }
+        if (t == 0)
+            __hip_atomic_store(&p.tickets[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+    const bool cvec = p.c_vec != 0;
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+                int dm, dn;
+                acc_coord<C::MI>(lane, g, dm, dn);
+                const int m = m0 + wm0 + fm * C::MI + dm;
+                const int n = n0 + wn0 + fn * C::MI + dn;
+                if (m < p.M)
+                    store4<C::DT>(Cb, (int64_t)m * p.N + n, n, p.N, cvec,
+                                  acc.v[fn][fm][4 * g], acc.v[fn][fm][4 * g + 1],
+                                  acc.v[fn][fm][4 * g + 2], acc.v[fn][fm][4 * g + 3]);
+            }
+}
+
+}  // namespace vxk

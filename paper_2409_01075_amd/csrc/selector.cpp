@@ -1,0 +1,176 @@
+// Runtime strategy selection (Section 5.2 and Section 6.2): an analytical cost
+// model evaluated per call over the precompiled candidates, with no profiling
+// and no shape samples.
+//
+// Cost of one candidate, bottom-up through the levels of the hierarchy:
+//   level 0 (wavefront)  temporal loop over the Kb/k0 MFMA steps of one K step:
+//                        T_Load  = fragment bytes read from LDS / LDS share,
+//                        Cost_-1 = MFMA time of the wavefronts' tiles,
+//                        no store (accumulators stay in registers)       Eq. 2
+//   level 1 (workgroup)  temporal loop over the n_k K steps of one slice:
+//                        T_Load  = load latency + tile bytes / L2->CU share,
+//                        Cost_0  = level-0 cost, T_Store = epilogue bytes
+//                        (+ split-K partial traffic and arrival counter)   Eq. 2
+//   level 2 (grid)       parallel loop over tiles x slices x batch:
+//                        F = ceil(workgroups / (CUs x resident WGs per CU)) Eq. 3
+//                        Cost_2 = F x T_temporal(level 1)                  Eq. 4
+// The call's cost adds the dispatch constant and is floored by the
+// compulsory HBM traffic at peak bandwidth.  The plan is the argmin (Eq. 1).
+#include <math.h>
+
+#include <algorithm>
+
+#include "vx_internal.h"
+
+extern "C" double vx_cost_temporal(double t_load, int64_t trips, double cost_lower, double t_store)
+{
+    if (trips <= 0)
+        return t_store;
+    return t_load + (double)(trips - 1) * std::max(t_load, cost_lower) + cost_lower + t_store;
+}
+
+extern "C" int64_t vx_cost_parallel_factor(int64_t parallel, int64_t units)
+{
+    if (parallel < 0 || units < 1)
+        return -1;
+    return (parallel + units - 1) / units;
+}
+
+static int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int vxi_group_m(int64_t tiles_m, int64_t tiles_n)
+{
+    // Walk 8 tile rows together when the grid is wide enough to need it.
+    (void)tiles_n;
+    return (int)std::max<int64_t>(1, std::min<int64_t>(8, tiles_m));
+}
+
+// Splits considered for K (the grid-level share of the reduction loop).
+static const int kSplits[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32};
+
+double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k, int split,
+                const VxLimits& lim, int* k_per_split)
+{
+    if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || split < 1)
+        return -1.0;
+    const int eb = sh.dt == VX_F32 ? 4 : 2;
+    const int64_t tiles_m = cdiv(sh.M, k.mb), tiles_n = cdiv(sh.N, k.nb);
+    const int64_t tiles = tiles_m * tiles_n * sh.batch;
+    int64_t kps = 0, nk = 0;
+    if (sh.K == 0) {
+        if (split != 1)
+            return -1.0;
+    } else {
+        kps = cdiv(cdiv(sh.K, split), k.kb) * k.kb;
+        if (cdiv(sh.K, kps) != split)       // a slice would be empty
+            return -1.0;
+        nk = kps / k.kb;
+    }
+    if (kps > INT32_MAX || tiles > INT32_MAX)
+        return -1.0;
+    const int64_t units = tiles * split;
+    if (units > INT32_MAX)
+        return -1.0;
+    if (split > 1) {
+        if (tiles > lim.max_tickets)
+            return -1.0;
+        if ((double)tiles * split * k.mb * k.nb * 4.0 > (double)lim.ws_bytes)
+            return -1.0;
+    }
+    if (k_per_split)
+        *k_per_split = (int)kps;
+
+    // Resident workgroups per CU: the tighter of the LDS and register budgets.
+    const int waves = k.wm * k.wn;
+    const int regs = ((k.vgprs + 7) / 8) * 8 + ((k.agprs + 7) / 8) * 8;
+    int waves_simd = regs > 0 ? hw.vgprs_per_lane / regs : hw.max_waves_per_simd;
+    waves_simd = std::max(1, std::min(waves_simd, hw.max_waves_per_simd));
+    const int by_regs = std::max(1, waves_simd * hw.simd_per_cu / waves);
+    const int by_lds = std::max(1, hw.lds_bytes_per_cu / std::max(1, k.lds_bytes));
+    const int occ = std::min(by_regs, by_lds);
+    const int64_t slots = (int64_t)hw.num_cu * occ;
+
+    // Level 2: wave quantisation over the device (Eq. 3).
+    const int64_t F = vx_cost_parallel_factor(units, slots);
+    const int64_t active = std::min(units, slots);
+    const double per_cu = (double)cdiv(active, hw.num_cu);
+
+    // Level 0: one K step of MFMAs fed from LDS (Eq. 2 over the Kb/k0 sub-steps).
+    const double flop_clk = sh.dt == VX_F32 ? hw.mfma_flop_clk_cu_f32 : hw.mfma_flop_clk_cu_f16;
+    const double rate_wg = flop_clk * hw.clock_ghz *
+                           std::min((double)waves / hw.simd_per_cu, 1.0 / per_cu);   // FLOP/ns
+    const int kstep = k.mfma_k * (sh.dt == VX_F32 ? 4 : 1);  // fp32 loads 4 MFMA steps at once
+    const int64_t sub = std::max<int64_t>(1, k.kb / kstep);
+    const double c_mfma = 2.0 * k.mb * k.nb * kstep / rate_wg;
+    const double lds_bw = hw.lds_bytes_clk_cu * hw.clock_ghz / per_cu;             // B/ns
+    const double t_lds = (double)waves * ((double)k.mb / k.wm + (double)k.nb / k.wn) * kstep * eb / lds_bw;
+    const double cost0 = vx_cost_temporal(t_lds, sub, c_mfma, 0.0);
+
+    // Level 1: the K loop of one workgroup (Eq. 2 over n_k K steps).
+    const double bw_wg = hw.l2_bytes_clk_cu * hw.clock_ghz / per_cu;                // B/ns
+    const double load_factor = k.vec ? 1.0 : 4.0;   // element-wise loads: 8x the instructions
+    const double t_load = hw.mem_latency_ns + (double)(k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
+    double t_store = (double)k.mb * k.nb * eb / bw_wg;
+    if (split > 1) {
+        const double part = (double)k.mb * k.nb * 4.0 / bw_wg;
+        t_store += part + hw.atomic_latency_ns + hw.mem_latency_ns + (double)(split - 1) * part;
+    }
+    const double t1 = vx_cost_temporal(t_load, nk, cost0, t_store);
+
+    // Level 2 (Eq. 4), dispatch constant, compulsory-traffic floor.
+    const double cost2 = (double)F * t1;
+    const double bytes_min = (double)sh.batch * ((double)sh.M * sh.K + (double)sh.K * sh.N + (double)sh.M * sh.N) * eb;
+    const double floor_ns = bytes_min / hw.hbm_gbps;
+    return hw.launch_ns + std::max(cost2, floor_ns);
+}
+
+vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim, int forced_id,
+                     int forced_split, vx_plan* out)
+{
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    double best = INFINITY;
+    int best_id = -1, best_split = 0, best_kps = 0;
+    for (int i = 0; i < n; ++i) {
+        const vx_kernel_info& k = reg[i].info;
+        if (forced_id >= 0 && k.id != forced_id)
+            continue;
+        for (int s : kSplits) {
+            int split = s;
+            if (forced_split > 0) {
+                if (s != 1)
+                    break;
+                // a forced split runs as the number of non-empty slices it yields
+                const int64_t kps0 = cdiv(cdiv(std::max<int64_t>(sh.K, 1), forced_split), k.kb) * k.kb;
+                split = sh.K == 0 ? 1 : (int)cdiv(sh.K, kps0);
+            }
+            int kps = 0;
+            const double c = vxi_cost(hw, sh, k, split, lim, &kps);
+            if (c < 0.0)
+                continue;
+            if (c < best) {   // strict: ties keep the earlier (lower id, smaller split) candidate
+                best = c;
+                best_id = i;
+                best_split = split;
+                best_kps = kps;
+            }
+        }
+    }
+    if (best_id < 0)
+        return VX_ERR_NO_CANDIDATE;
+    const vx_kernel_info& k = reg[best_id].info;
+    vx_plan p;
+    p.kernel_id = k.id;
+    p.split_k = best_split;
+    p.k_per_split = best_kps;
+    p.c_vec = sh.c_vec;
+    p.tiles_m = cdiv(sh.M, k.mb);
+    p.tiles_n = cdiv(sh.N, k.nb);
+    p.grid = p.tiles_m * p.tiles_n * sh.batch * best_split;
+    p.group_m = vxi_group_m(p.tiles_m, p.tiles_n);
+    p.workspace_bytes = best_split > 1 ? (size_t)(p.tiles_m * p.tiles_n * sh.batch) * best_split * k.mb * k.nb * 4 : 0;
+    p.predicted_ns = best;
+    p.kernel = k;
+    *out = p;
+    return VX_OK;
+}

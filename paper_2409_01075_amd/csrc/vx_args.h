@@ -1,0 +1,20 @@
+// Launch arguments shared by the host launcher and the device kernels.
+#pragma once
+#include <stdint.h>
+
+struct VxGemmArgs {
+    const void* A;          // M x K row-major (lda = K), batch stride sA elements
+    const void* B;          // K x N row-major (ldb = N), batch stride sB (0 = broadcast)
+    void* C;                // M x N row-major (ldc = N), batch stride sC
+    int64_t sA, sB, sC;
+    int M, N, K;
+    int tiles_m, tiles_n;   // ceil(M / Mb), ceil(N / Nb)
+    int split;              // split-K factor s (>= 1)
+    int k_per_split;        // K extent of one slice, a multiple of Kb
+    int batch;
+    int group_m;            // tile rows walked together by the grid-level order
+    int num_xcd;            // workgroups are dispatched round-robin over this many XCDs
+    int c_vec;              // 1: C rows allow 4-element vector stores
+    float* ws;              // split-K partial tiles (split > 1), fp32
+    unsigned* tickets;      // one self-resetting arrival counter per output tile
+};

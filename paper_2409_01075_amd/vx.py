@@ -1,0 +1,220 @@
+"""Thin ctypes binding of libvx.so (argument marshalling only).
+
+The names mirror the C ABI in include/vx.h.  Every GEMM runs in the library's
+HIP kernels; there is no fallback: if libvx.so is missing or cannot be loaded
+this module raises.  PyTorch is used only to hand over device pointers and the
+current HIP stream.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libvx.so")
+
+VX_F32, VX_F16, VX_BF16 = 0, 1, 2
+STATUS = {0: "VX_OK", 1: "VX_ERR_INVALID_ARG", 2: "VX_ERR_UNSUPPORTED_DTYPE",
+          3: "VX_ERR_NO_CANDIDATE", 4: "VX_ERR_WORKSPACE", 5: "VX_ERR_HIP"}
+
+
+class vx_hwinfo(ctypes.Structure):
+    _fields_ = [("arch", ctypes.c_char * 32)] + [
+        (n, ctypes.c_int) for n in ("num_cu", "num_xcd", "simd_per_cu", "wave_size", "max_threads_per_wg",
+                                    "lds_bytes_per_cu", "vgprs_per_lane", "max_waves_per_simd")] + [
+        (n, ctypes.c_double) for n in ("clock_ghz", "hbm_gbps", "l2_bytes_per_xcd", "mall_bytes",
+                                       "mfma_flop_clk_cu_f16", "mfma_flop_clk_cu_f32", "l2_bytes_clk_cu",
+                                       "lds_bytes_clk_cu", "mem_latency_ns", "atomic_latency_ns",
+                                       "launch_ns")]
+
+
+class vx_kernel_info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in (
+        "id", "dtype", "mb", "nb", "kb", "wm", "wn", "mfma_m", "mfma_n", "mfma_k", "vec", "threads",
+        "lds_bytes", "vgprs", "agprs", "sgprs", "scratch_bytes", "enabled")]
+
+
+class vx_plan(ctypes.Structure):
+    _fields_ = [("kernel_id", ctypes.c_int), ("split_k", ctypes.c_int), ("k_per_split", ctypes.c_int),
+                ("c_vec", ctypes.c_int), ("tiles_m", ctypes.c_int64), ("tiles_n", ctypes.c_int64),
+                ("grid", ctypes.c_int64), ("group_m", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t),
+                ("predicted_ns", ctypes.c_double), ("kernel", vx_kernel_info)]
+
+
+class VxError(RuntimeError):
+    def __init__(self, status, what=""):
+        self.status = status
+        super().__init__("%s%s" % (what + ": " if what else "", STATUS.get(status, status)))
+
+
+_lib = None
+
+
+def lib():
+    """Loads libvx.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libvx.so not built: run `python -m paper_2409_01075_amd.build` "
+                           "(or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    L.vx_gemm.argtypes = [i64, i64, i64, i32, vp, vp, vp, vp]
+    L.vx_gemm.restype = i32
+    L.vx_gemm_batched.argtypes = [i64, i64, i64, i64, i32, vp, i64, vp, i64, vp, i64, vp]
+    L.vx_gemm_batched.restype = i32
+    L.vx_plan_query.argtypes = [i64, i64, i64, i64, i32, i64, i64, i64, ctypes.c_uint64, ctypes.POINTER(vx_plan)]
+    L.vx_plan_query.restype = i32
+    L.vx_plan_cost.argtypes = [i64, i64, i64, i64, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_double)]
+    L.vx_plan_cost.restype = i32
+    L.vx_cost_temporal.argtypes = [ctypes.c_double, i64, ctypes.c_double, ctypes.c_double]
+    L.vx_cost_temporal.restype = ctypes.c_double
+    L.vx_cost_parallel_factor.argtypes = [i64, i64]
+    L.vx_cost_parallel_factor.restype = i64
+    L.vx_get_hwinfo.argtypes = [ctypes.POINTER(vx_hwinfo)]
+    L.vx_get_hwinfo.restype = i32
+    L.vx_set_hwinfo_override.argtypes = [ctypes.POINTER(vx_hwinfo)]
+    L.vx_set_hwinfo_override.restype = i32
+    L.vx_registry_count.argtypes = []
+    L.vx_registry_count.restype = i32
+    L.vx_registry_get.argtypes = [i32, ctypes.POINTER(vx_kernel_info)]
+    L.vx_registry_get.restype = i32
+    L.vx_force_plan.argtypes = [i32, i32]
+    L.vx_force_plan.restype = i32
+    L.vx_set_workspace.argtypes = [vp, ctypes.c_size_t, vp]
+    L.vx_set_workspace.restype = i32
+    L.vx_status_string.argtypes = [i32]
+    L.vx_status_string.restype = ctypes.c_char_p
+    L.vx_version.argtypes = []
+    L.vx_version.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _chk(st, what):
+    if st != 0:
+        raise VxError(st, what)
+
+
+# ------------------------------------------------------------- raw ABI -----
+def vx_gemm(M, N, K, dtype, A, B, C, stream=None):
+    return lib().vx_gemm(M, N, K, dtype, A, B, C, stream)
+
+
+def vx_gemm_batched(batch, M, N, K, dtype, A, sA, B, sB, C, sC, stream=None):
+    return lib().vx_gemm_batched(batch, M, N, K, dtype, A, sA, B, sB, C, sC, stream)
+
+
+def vx_plan_query(batch, M, N, K, dtype, sA=None, sB=None, sC=None, base_align=256):
+    p = vx_plan()
+    st = lib().vx_plan_query(batch, M, N, K, dtype, M * K if sA is None else sA, K * N if sB is None else sB,
+                             M * N if sC is None else sC, base_align, ctypes.byref(p))
+    _chk(st, "vx_plan_query")
+    return p
+
+
+def vx_plan_cost(batch, M, N, K, dtype, kernel_id, split_k, vec_ok=1):
+    c = ctypes.c_double()
+    st = lib().vx_plan_cost(batch, M, N, K, dtype, kernel_id, split_k, vec_ok, ctypes.byref(c))
+    return st, c.value
+
+
+def vx_cost_temporal(t_load, trips, cost_lower, t_store):
+    return lib().vx_cost_temporal(t_load, trips, cost_lower, t_store)
+
+
+def vx_cost_parallel_factor(parallel, units):
+    return lib().vx_cost_parallel_factor(parallel, units)
+
+
+def vx_get_hwinfo():
+    h = vx_hwinfo()
+    _chk(lib().vx_get_hwinfo(ctypes.byref(h)), "vx_get_hwinfo")
+    return h
+
+
+def vx_set_hwinfo_override(hw):
+    return lib().vx_set_hwinfo_override(None if hw is None else ctypes.byref(hw))
+
+
+def vx_registry_count():
+    return lib().vx_registry_count()
+
+
+def vx_registry_get(i):
+    k = vx_kernel_info()
+    _chk(lib().vx_registry_get(i, ctypes.byref(k)), "vx_registry_get")
+    return k
+
+
+def vx_force_plan(kernel_id, split_k=0):
+    return lib().vx_force_plan(kernel_id, split_k)
+
+
+def vx_set_workspace(ptr, nbytes, stream=None):
+    return lib().vx_set_workspace(ptr, nbytes, stream)
+
+
+def vx_status_string(s):
+    return lib().vx_status_string(s).decode()
+
+
+def vx_version():
+    return lib().vx_version().decode()
+
+
+def mi355x_hwinfo():
+    """The gfx950 description the library builds from the device, as a literal
+    (for planning on a host without a GPU)."""
+    h = vx_hwinfo()
+    h.arch = b"gfx950"
+    h.num_cu, h.num_xcd, h.simd_per_cu, h.wave_size = 256, 8, 4, 64
+    h.max_threads_per_wg, h.lds_bytes_per_cu, h.vgprs_per_lane, h.max_waves_per_simd = 1024, 160 * 1024, 512, 8
+    h.clock_ghz, h.hbm_gbps = 2.4, 8000.0
+    h.l2_bytes_per_xcd, h.mall_bytes = 4.0 * 2 ** 20, 256.0 * 2 ** 20
+    h.mfma_flop_clk_cu_f16, h.mfma_flop_clk_cu_f32 = 4096.0, 256.0
+    h.l2_bytes_clk_cu, h.lds_bytes_clk_cu = 64.0, 128.0
+    h.mem_latency_ns, h.atomic_latency_ns, h.launch_ns = 900.0, 1200.0, 2000.0
+    return h
+
+
+# ------------------------------------------------------ torch helpers -------
+def _torch_dtype_code(t):
+    import torch
+    return {torch.float32: VX_F32, torch.float16: VX_F16, torch.bfloat16: VX_BF16}[t.dtype]
+
+
+def _stream_ptr(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def gemm(A, B, out=None, stream=None):
+    """C = A @ B for 2-D row-major device tensors (contiguous)."""
+    import torch
+    M, K = A.shape
+    K2, N = B.shape
+    if K2 != K or A.dtype != B.dtype or not A.is_contiguous() or not B.is_contiguous():
+        raise ValueError("gemm expects contiguous A (M x K), B (K x N) of one dtype")
+    C = torch.empty((M, N), dtype=A.dtype, device=A.device) if out is None else out
+    _chk(vx_gemm(M, N, K, _torch_dtype_code(A), A.data_ptr(), B.data_ptr(), C.data_ptr(), _stream_ptr(stream)),
+         "vx_gemm")
+    return C
+
+
+def bmm(A, B, out=None, stream=None):
+    """C[b] = A[b] @ B[b] for contiguous 3-D device tensors; B may be 2-D (broadcast)."""
+    import torch
+    bt, M, K = A.shape
+    if B.dim() == 2:
+        K2, N = B.shape
+        sB = 0
+    else:
+        _, K2, N = B.shape
+        sB = K2 * N
+    if K2 != K or A.dtype != B.dtype or not A.is_contiguous() or not B.is_contiguous():
+        raise ValueError("bmm expects contiguous operands of one dtype")
+    C = torch.empty((bt, M, N), dtype=A.dtype, device=A.device) if out is None else out
+    _chk(vx_gemm_batched(bt, M, N, K, _torch_dtype_code(A), A.data_ptr(), M * K, B.data_ptr(), sB,
+                         C.data_ptr(), M * N, _stream_ptr(stream)), "vx_gemm_batched")
+    return C

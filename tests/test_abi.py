@@ -1,0 +1,223 @@
+"""Host-side checks of the C-ABI library: it loads, exports every declared
+symbol with the declared struct layouts, validates arguments before touching
+the GPU, and its registry satisfies the candidate-generation invariants."""
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+from paper_2409_01075_amd import vx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vx.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(vx_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    L = vx.lib()
+    names = _declared_functions()
+    assert len(names) >= 14
+    missing = [n for n in names if not hasattr(L, n)]
+    assert not missing, missing
+    # and nm agrees that they are real dynamic exports
+    out = subprocess.run(["nm", "-D", "--defined-only", vx.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (vx_[a-z_0-9]+)\b", out))
+    assert set(names) <= exported, set(names) - exported
+
+
+def test_struct_layouts_match_header(tmp_path):
+    import ctypes
+    probe = tmp_path / "probe.c"
+    probe.write_text("""
+#include <stdio.h>
+#include <stddef.h>
+#include "vx.h"
+int main(void) {
+  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(vx_hwinfo), sizeof(vx_kernel_info), sizeof(vx_plan),
+         offsetof(vx_plan, predicted_ns), offsetof(vx_plan, kernel), offsetof(vx_hwinfo, clock_ghz));
+  return 0;
+}
+""")
+    exe = tmp_path / "probe"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(probe), "-o", str(exe)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
+    want = [ctypes.sizeof(vx.vx_hwinfo), ctypes.sizeof(vx.vx_kernel_info), ctypes.sizeof(vx.vx_plan),
+            vx.vx_plan.predicted_ns.offset, vx.vx_plan.kernel.offset, vx.vx_hwinfo.clock_ghz.offset]
+    assert got == want
+
+
+def test_argument_errors_without_gpu():
+    F16 = vx.VX_F16
+    assert vx.vx_gemm(4, 4, 4, 7, 16, 1024, 4096, None) == 2          # unsupported dtype
+    assert vx.vx_gemm(-1, 4, 4, F16, 16, 1024, 4096, None) == 1       # negative M
+    assert vx.vx_gemm(4, -4, 4, F16, 16, 1024, 4096, None) == 1
+    assert vx.vx_gemm(4, 4, -4, F16, 16, 1024, 4096, None) == 1
+    assert vx.vx_gemm(4, 4, 4, F16, None, 1024, 4096, None) == 1      # NULL A with M*K > 0
+    assert vx.vx_gemm(4, 4, 4, F16, 16, None, 4096, None) == 1
+    assert vx.vx_gemm(4, 4, 4, F16, 16, 1024, None, None) == 1
+    assert vx.vx_gemm(4, 4, 4, F16, 4096, 1024, 4100, None) == 1      # C overlaps A
+    assert vx.vx_gemm(4, 4, 4, F16, 16, 4096, 4090, None) == 1        # C overlaps B
+    assert vx.vx_gemm(2 ** 31, 4, 4, F16, 16, 1024, 4096, None) == 1  # beyond int32 dims
+    assert vx.vx_gemm_batched(-1, 4, 4, 4, F16, 16, 16, 1024, 16, 4096, 16, None) == 1
+    assert vx.vx_gemm_batched(2, 4, 4, 4, F16, 16, 16, 1024, 16, 4096, 8, None) == 1  # C batches overlap
+    assert vx.vx_gemm_batched(2, 4, 4, 4, F16, 16, -16, 1024, 16, 4096, 16, None) == 1
+    # empty problems are no-ops that never reach the device
+    assert vx.vx_gemm(0, 4, 4, F16, None, 1024, None, None) == 0
+    assert vx.vx_gemm(4, 0, 4, F16, 16, None, None, None) == 0
+    assert vx.vx_gemm_batched(0, 4, 4, 4, F16, None, 16, None, 16, None, 16, None) == 0
+    for s in range(6):
+        assert vx.vx_status_string(s).startswith("VX_")
+
+
+def test_cost_model_golden_cases():
+    path = os.path.join(ROOT, "tests", "golden", "cost_model_cases.txt")
+    n = 0
+    for ln in open(path):
+        if not ln.strip() or ln.startswith("#"):
+            continue
+        f = ln.split()
+        if f[0] == "temporal":
+            got = vx.vx_cost_temporal(float(f[1]), int(f[2]), float(f[3]), float(f[4]))
+            assert got == pytest.approx(float(f[5]), abs=0, rel=1e-15), ln
+        else:
+            assert vx.vx_cost_parallel_factor(int(f[1]), int(f[2])) == int(f[3]), ln
+        n += 1
+    assert n >= 10
+    assert vx.vx_cost_parallel_factor(5, 0) == -1
+
+
+def test_registry_invariants():
+    n = vx.vx_registry_count()
+    assert n > 0
+    isa = {0: {(16, 16, 4), (32, 32, 2)}, 1: {(16, 16, 32), (32, 32, 16)}, 2: {(16, 16, 32), (32, 32, 16)}}
+    seen = set()
+    for i in range(n):
+        k = vx.vx_registry_get(i)
+        assert k.id == i
+        assert (k.mfma_m, k.mfma_n, k.mfma_k) in isa[k.dtype]                  # L0: FilterByISA
+        mw, nw = k.mb // k.wm, k.nb // k.wn
+        assert k.mb == k.wm * mw and k.nb == k.wn * nw                          # L2 multiple of L1
+        assert mw % k.mfma_m == 0 and nw % k.mfma_n == 0                        # L1 multiple of L0
+        assert k.kb % k.mfma_k == 0
+        assert k.threads == 64 * k.wm * k.wn <= 1024
+        assert k.lds_bytes <= 160 * 1024
+        assert k.enabled == (1 if k.scratch_bytes == 0 else 0)
+        assert k.vgprs + k.agprs <= 512 and k.vgprs > 0
+        seen.add((k.dtype, k.vec))
+    assert seen == {(d, v) for d in (0, 1, 2) for v in (0, 1)}
+    enabled = sum(vx.vx_registry_get(i).enabled for i in range(n))
+    assert enabled >= 0.9 * n
+
+
+def test_candidate_generator_properties():
+    sys.path.insert(0, os.path.join(ROOT, "paper_2409_01075_amd", "csrc"))
+    try:
+        import candidates as C
+    finally:
+        sys.path.pop(0)
+    for dt in ("f16", "bf16", "f32"):
+        l0, _ = C.generate_candidates_for_layer(0, dt)
+        assert set(l0) == set(C.GFX950["mfma"][dt])
+        l1, link1 = C.generate_candidates_for_layer(1, dt)
+        for c in l1:
+            assert link1[c] and all(c[0] % p[0] == 0 and c[1] % p[1] == 0 for p in link1[c])
+            assert 4 <= c[0] * c[1] // 64 <= 128
+        l2, link2 = C.generate_candidates_for_layer(2, dt)
+        for c in l2:
+            mb, nb, kb, wm, wn, mi = c
+            for (w, l0c) in link2[c]:
+                assert w in l1 and mb == wm * w[0] and nb == wn * w[1]
+                assert kb % l0c[2] == 0 and l0c in l0
+            assert C.lds_bytes(dt, mb, nb, kb) <= C.GFX950["lds_bytes"]
+    reg = C.registry()
+    assert len(reg) == vx.vx_registry_count()
+
+
+@pytest.fixture
+def mi355x_override():
+    assert vx.vx_set_hwinfo_override(vx.mi355x_hwinfo()) == 0
+    yield
+    assert vx.vx_set_hwinfo_override(None) == 0
+
+
+def _shapes():
+    import numpy as np
+    g = np.random.default_rng(5)
+    out = [(1, 1, 1, 1), (1, 77, 96, 80), (1, 1, 768, 768), (1, 512, 768, 768), (1, 8192, 11008, 4096),
+           (192, 1000, 1000, 64), (192, 1000, 64, 1000), (1, 5, 3, 0), (3, 7, 9, 11)]
+    for _ in range(60):
+        out.append((int(g.integers(1, 4)), int(g.integers(1, 5000)), int(g.integers(1, 5000)),
+                    int(g.integers(0, 12000))))
+    return out
+
+
+def test_selector_plans_cover_and_are_feasible(mi355x_override):
+    for dt in (0, 1, 2):
+        for (b, M, N, K) in _shapes():
+            for align in (256, 2):
+                p = vx.vx_plan_query(b, M, N, K, dt, base_align=align)
+                k = p.kernel
+                assert k.enabled and k.dtype == dt
+                if align == 2:
+                    assert k.vec == 0
+                if k.vec:
+                    ve = 8 if dt else 4
+                    assert K % ve == 0 and N % ve == 0
+                assert p.tiles_m * k.mb >= M and (p.tiles_m - 1) * k.mb < M
+                assert p.tiles_n * k.nb >= N and (p.tiles_n - 1) * k.nb < N
+                assert p.grid == p.tiles_m * p.tiles_n * b * p.split_k
+                if K == 0:
+                    assert p.split_k == 1
+                else:
+                    assert p.k_per_split % k.kb == 0
+                    assert p.split_k * p.k_per_split >= K > (p.split_k - 1) * p.k_per_split
+                if p.split_k > 1:
+                    assert p.workspace_bytes == p.tiles_m * p.tiles_n * b * p.split_k * k.mb * k.nb * 4
+                    assert p.workspace_bytes <= 64 * 2 ** 20
+                    assert p.tiles_m * p.tiles_n * b <= 65536
+                assert p.predicted_ns > 0
+                # deterministic
+                q = vx.vx_plan_query(b, M, N, K, dt, base_align=align)
+                assert (q.kernel_id, q.split_k) == (p.kernel_id, p.split_k)
+
+
+def test_selector_is_the_argmin_of_the_cost_model(mi355x_override):
+    """Equation 1: the chosen plan has the lowest modelled cost of every
+    (kernel, split) pair, found here by brute force through vx_plan_cost."""
+    n = vx.vx_registry_count()
+    splits = [1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32]
+    for dt, (b, M, N, K) in [(1, (1, 1, 768, 768)), (1, (1, 300, 768, 768)), (2, (1, 8192, 4096, 4096)),
+                             (2, (192, 333, 333, 64)), (2, (192, 336, 336, 64)), (0, (1, 77, 96, 80)), (2, (1, 16, 11008, 4096))]:
+        p = vx.vx_plan_query(b, M, N, K, dt)
+        ve = 8 if dt else 4
+        vec_ok = int(K % ve == 0 and N % ve == 0)
+        best = min(c for i in range(n) for s in splits
+                   for st, c in [vx.vx_plan_cost(b, M, N, K, dt, i, s, vec_ok)] if st == 0)
+        assert p.predicted_ns == pytest.approx(best, rel=1e-12)
+        st, c = vx.vx_plan_cost(b, M, N, K, dt, p.kernel_id, p.split_k, vec_ok)
+        assert st == 0 and c == pytest.approx(p.predicted_ns, rel=1e-12)
+
+
+def test_selector_responds_to_hardware(mi355x_override):
+    """A device with a quarter of the CUs gets plans with no more workgroups
+    per CU slot wasted: the model must see the smaller machine."""
+    h = vx.mi355x_hwinfo()
+    p_full = vx.vx_plan_query(1, 16, 4096, 4096, 2)
+    h.num_cu = 64
+    assert vx.vx_set_hwinfo_override(h) == 0
+    p_small = vx.vx_plan_query(1, 16, 4096, 4096, 2)
+    assert p_small.predicted_ns > p_full.predicted_ns
+    assert p_small.grid <= p_full.grid
+
+
+def test_force_plan_validation():
+    assert vx.vx_force_plan(vx.vx_registry_count(), 1) == 3
+    assert vx.vx_force_plan(0, 2) == 0
+    assert vx.vx_force_plan(-1, 0) == 0

@@ -1,0 +1,263 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bounds (see oracle/tolerance.py): fp16/bf16 |C-Cref| <= 4e-3*Mag + 1e-6,
+fp32 1e-5*Mag elementwise and normwise; integer-valued inputs bit-exact.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import tolerance
+from paper_2409_01075_amd import inputs as I
+from paper_2409_01075_amd import vx
+
+from .gpu_util import from_dev, run_gemm, run_batched
+
+pytestmark = pytest.mark.gpu
+
+DTS = [I.F32, I.F16, I.BF16]
+
+
+@pytest.fixture(autouse=True)
+def _unforce():
+    vx.vx_force_plan(-1, 0)
+    yield
+    vx.vx_force_plan(-1, 0)
+
+
+def test_single_f32_77x96x80():
+    A, B = I.single_f32(0)
+    C = run_gemm(A, B, I.F32)
+    ref, mag = oracle.gemm(A, B, I.F32)
+    tolerance.check(C, ref, mag, I.F32, "fp32 77x96x80")
+
+
+@pytest.mark.parametrize("M", [1, 2, 3, 7, 8, 15, 16, 17, 31, 33, 63, 64, 65, 100, 127, 129, 200, 255,
+                               256, 257, 300, 383, 384, 385, 448, 511, 512])
+def test_sweep_f16(M):
+    A, B = I.sweep_f16(M)
+    C = run_gemm(A, B, I.F16)
+    ref, mag = oracle.gemm(A, B, I.F16)
+    tolerance.check(C, ref, mag, I.F16, "fp16 M=%d" % M)
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_identity_permutation_exact(code):
+    g = I.rng(100 + code)
+    for M, N in [(77, 96), (17, 40), (1, 9), (130, 264)]:
+        K = M
+        B = I.small_int(g, (K, N), code, -8, 8)
+        P = I.to_storage(np.eye(M)[g.permutation(M)], code)
+        tolerance.check_exact(run_gemm(P, B, code), oracle.gemm(P, B, code)[0], code, "perm %d" % M)
+        A = I.small_int(g, (M, N), code, -8, 8)
+        E = I.to_storage(np.eye(N), code)
+        tolerance.check_exact(run_gemm(A, E, code), oracle.gemm(A, E, code)[0], code, "B=I %d" % M)
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_random_shapes_integer_exact(code):
+    g = I.rng(200 + code)
+    for _ in range(25):
+        M, N, K = (int(v) for v in g.integers(1, 301, size=3))
+        r = max(1, min(8, I.exact_range(K, code)))
+        lo = -r
+        A = I.small_int(g, (M, K), code, lo, r)
+        B = I.small_int(g, (K, N), code, lo, r)
+        ref = oracle.gemm(A, B, code, with_mag=False)
+        # inputs with K*r*r beyond the exact range still must be within bounds
+        if K * r * r <= 2 ** {0: 24, 1: 11, 2: 8}[code]:
+            tolerance.check_exact(run_gemm(A, B, code), ref, code, "int %dx%dx%d" % (M, N, K))
+        else:
+            ref, mag = oracle.gemm(A, B, code)
+            tolerance.check(run_gemm(A, B, code), ref, mag, code, "int %dx%dx%d" % (M, N, K))
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_rank1_closed_form(code):
+    for K in (1, 5, 77, 300):
+        M, N = 35, 70
+        A = I.to_storage(np.ones((M, K)), code)
+        Bk = np.tile(((np.arange(K) % 5) - 2.0)[:, None], (1, N))
+        C = run_gemm(A, I.to_storage(Bk, code), code)
+        q, r = divmod(K, 5)
+        want = I.to_storage(np.full((M, N), r * (r - 1) / 2 - 2 * r), code)
+        assert np.array_equal(C, want)
+
+
+def test_rne_ties_on_device():
+    # fp16: 2048 + 1 = 2049 -> 2048; 2048 + 3 = 2051 -> 2052 (ties to even)
+    A = I.to_storage(np.ones((1, 2)), I.F16)
+    B = I.to_storage(np.array([[2048.0, 2048.0], [1.0, 3.0]]), I.F16)
+    C = run_gemm(A, B, I.F16)
+    assert [int(v) for v in C[0]] == [0x6800, 0x6802]
+    A = I.to_storage(np.ones((1, 2)), I.BF16)
+    B = I.to_storage(np.array([[256.0, 256.0], [1.0, 3.0]]), I.BF16)
+    C = run_gemm(A, B, I.BF16)
+    assert [int(v) for v in C[0]] == [0x4380, 0x4382]
+
+
+def test_fp16_subnormal_output():
+    A = I.to_storage(np.full((3, 1), 2.0 ** -12), I.F16)
+    B = I.to_storage(np.full((1, 5), 2.0 ** -12), I.F16)
+    C = run_gemm(A, B, I.F16)
+    assert np.all(C == 0x0001), C   # 2^-24, the smallest fp16 subnormal
+
+
+def test_k_zero_writes_zeros_and_empty_is_noop():
+    import torch
+    from .gpu_util import empty_out
+    for code in DTS:
+        C = empty_out((5, 7), code, fill_bits=0x1234)
+        A = empty_out((5, 0), code)
+        B = empty_out((0, 7), code)
+        st = vx.vx_gemm(5, 7, 0, code, A.data_ptr() or 0, B.data_ptr() or 0, C.data_ptr(),
+                        torch.cuda.current_stream().cuda_stream)
+        assert st == 0
+        torch.cuda.synchronize()
+        assert not C.float().abs().sum().item()
+        C2 = empty_out((3, 4), code, fill_bits=0x1234)
+        st = vx.vx_gemm(0, 4, 6, code, 0, C.data_ptr(), C2.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        assert st == 0
+        torch.cuda.synchronize()
+        bits = from_dev(C2, code)
+        assert np.all((bits.view(np.uint32) if code == 0 else bits) == 0x1234)
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_batched_and_broadcast(code):
+    g = I.rng(300 + code)
+    bt, M, N, K = 5, 37, 45, 29
+    A = I.normal(g, (bt, M, K), code)
+    B = I.normal(g, (bt, K, N), code)
+    C = run_batched(A, M * K, B, K * N, code, bt, M, N, K).reshape(bt, M, N)
+    ref, mag = oracle.gemm(A, B, code, M=M, N=N, K=K, batch=bt)
+    tolerance.check(C, ref, mag, code, "batched")
+    C = run_batched(A, M * K, B[0], 0, code, bt, M, N, K).reshape(bt, M, N)
+    ref, mag = oracle.gemm(A, B[0], code, M=M, N=N, K=K, batch=bt, sB=0)
+    tolerance.check(C, ref, mag, code, "broadcast B")
+
+
+def _kernel_cases():
+    n = vx.vx_registry_count()
+    return [vx.vx_registry_get(i) for i in range(n)]
+
+
+def _shape_for(k, extra_m=3, extra_n=5, extra_k=8):
+    """A ragged shape spanning 2 x 2 tiles and a K tail for kernel k."""
+    M = 2 * k.mb + extra_m
+    N = k.nb + (8 if k.vec else extra_n)
+    K = 2 * k.kb + (8 if k.vec else extra_k + 1)
+    return M, N, K
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_every_kernel_integer_exact(code):
+    """Forces each compiled candidate of this dtype on a ragged multi-tile shape."""
+    g = I.rng(400 + code)
+    ran = 0
+    for k in _kernel_cases():
+        if k.dtype != code or not k.enabled:
+            continue
+        M, N, K = _shape_for(k)
+        r = max(1, min(4, I.exact_range(K, code)))
+        A = I.small_int(g, (M, K), code, -r, r)
+        B = I.small_int(g, (K, N), code, -r, r)
+        assert vx.vx_force_plan(k.id, 1) == 0
+        C = run_gemm(A, B, code)
+        vx.vx_force_plan(-1, 0)
+        tolerance.check_exact(C, oracle.gemm(A, B, code, with_mag=False), code,
+                              "kernel %d %s" % (k.id, (k.mb, k.nb, k.kb, k.wm, k.wn, k.mfma_m, k.vec)))
+        ran += 1
+    assert ran > 0
+
+
+@pytest.mark.parametrize("code", DTS)
+@pytest.mark.parametrize("split", [2, 3, 5, 8])
+def test_split_k_integer_exact(code, split):
+    g = I.rng(500 + 10 * code + split)
+    picked = [k for k in _kernel_cases() if k.dtype == code and k.enabled][::7]
+    for k in picked:
+        M, N, _ = _shape_for(k)
+        K = split * k.kb + (8 if k.vec else 5)
+        r = max(1, min(4, I.exact_range(K, code)))
+        A = I.small_int(g, (M, K), code, -r, r)
+        B = I.small_int(g, (K, N), code, -r, r)
+        assert vx.vx_force_plan(k.id, split) == 0
+        C1 = run_gemm(A, B, code)
+        C2 = run_gemm(A, B, code)      # counters must have reset themselves
+        vx.vx_force_plan(-1, 0)
+        ref = oracle.gemm(A, B, code, with_mag=False)
+        tolerance.check_exact(C1, ref, code, "kernel %d split %d" % (k.id, split))
+        assert np.array_equal(C1, C2)
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_split_k_random_within_bound(code):
+    g = I.rng(600 + code)
+    M, N, K = 45, 72, 1000
+    A = I.normal(g, (M, K), code)
+    B = I.normal(g, (K, N), code, 0.02)
+    ref, mag = oracle.gemm(A, B, code)
+    for k in [k for k in _kernel_cases() if k.dtype == code and k.enabled and k.vec][::11]:
+        for split in (2, 4, 7):
+            assert vx.vx_force_plan(k.id, split) == 0
+            C = run_gemm(A, B, code)
+            tolerance.check(C, ref, mag, code, "kernel %d split %d" % (k.id, split))
+    vx.vx_force_plan(-1, 0)
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_guard_bands_and_canaries(code):
+    """NaN guard bands around A and B (an out-of-bounds read would leak NaN into
+    C) and canaries around C (an out-of-bounds write would change them)."""
+    import torch
+    from .gpu_util import to_dev, empty_out
+    g = I.rng(700 + code)
+    nan = 0x7fc0 if code else 0x7fc00000
+    for (M, N, K) in [(77, 96, 80), (33, 41, 19), (130, 264, 520), (5, 3, 1)]:
+        pad = 4096
+        A = I.normal(g, (M, K), code)
+        B = I.normal(g, (K, N), code)
+        bits_dt = np.uint32 if code == 0 else np.uint16
+        Ag = np.full(M * K + 2 * pad, nan, dtype=bits_dt)
+        Ag[pad:pad + M * K] = A.reshape(-1).view(bits_dt)
+        Bg = np.full(K * N + 2 * pad, nan, dtype=bits_dt)
+        Bg[pad:pad + K * N] = B.reshape(-1).view(bits_dt)
+        At = to_dev(Ag.view(np.float32) if code == 0 else Ag, code)
+        Bt = to_dev(Bg.view(np.float32) if code == 0 else Bg, code)
+        Ct = empty_out((M * N + 2 * pad,), code, fill_bits=0x5a5a)
+        for sp in (1, 3):
+            ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and not k.vec]
+            for k in [None] + ks[::13]:
+                vx.vx_force_plan(-1 if k is None else k.id, sp)
+                st = vx.vx_gemm(M, N, K, code, At.data_ptr() + pad * At.element_size(),
+                                Bt.data_ptr() + pad * Bt.element_size(), Ct.data_ptr() + pad * Ct.element_size(),
+                                torch.cuda.current_stream().cuda_stream)
+                vx.vx_force_plan(-1, 0)
+                assert st == 0
+                torch.cuda.synchronize()
+                out = from_dev(Ct, code)
+                raw = out.view(np.uint32) if code == 0 else out
+                assert np.all(raw[:pad] == 0x5a5a) and np.all(raw[pad + M * N:] == 0x5a5a)
+                ref, mag = oracle.gemm(A, B, code)
+                tolerance.check(out[pad:pad + M * N].reshape(M, N), ref, mag, code, "guard %s" % ((M, N, K),))
+
+
+def test_deterministic_bitwise():
+    g = I.rng(800)
+    A = I.normal(g, (300, 4096), I.BF16)
+    B = I.normal(g, (4096, 1000), I.BF16, 0.02)
+    C1 = run_gemm(A, B, I.BF16)
+    for _ in range(3):
+        assert np.array_equal(C1, run_gemm(A, B, I.BF16))
+
+
+def test_error_codes_on_device():
+    import torch
+    s = torch.cuda.current_stream().cuda_stream
+    x = torch.zeros(64, device="cuda", dtype=torch.float16)
+    assert vx.vx_gemm(4, 4, 4, 9, x.data_ptr(), x.data_ptr() + 64, x.data_ptr() + 96, s) == 2
+    assert vx.vx_gemm(4, 4, -1, 1, x.data_ptr(), x.data_ptr(), x.data_ptr(), s) == 1
+    # C overlapping A
+    assert vx.vx_gemm(4, 4, 4, 1, x.data_ptr(), x.data_ptr() + 64, x.data_ptr() + 8, s) == 1
+    assert vx.vx_force_plan(10 ** 6, 1) == 3
