@@ -86,6 +86,8 @@ typedef struct vx_kernel_info {
     int wm, wn;                    /* wavefront grid; wavefront tile = (mb/wm) x (nb/wn) */
     int mfma_m, mfma_n, mfma_k;    /* instruction tile */
     int vec;                       /* 1: 16-byte vector loads (aligned operands only) */
+    int family;                    /* 0: loads staged through registers, 1: direct-to-LDS DMA */
+    int stages;                    /* LDS ring depth (K steps in flight + 1) */
     int threads;
     int lds_bytes;
     int vgprs, agprs, sgprs;       /* from the compiler's resource report of this build */

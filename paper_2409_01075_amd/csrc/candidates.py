@@ -14,16 +14,28 @@ Levels (Table 1, GPU rows):
       multiples of an L1 tile (FilterByMultiples).
 The grid level has no tile of its own: it is the runtime parallel loop.
 
+Two level-1 load strategies exist (the Load stage of Algorithm 1 at the
+workgroup level):
+  * "dma": fp16/bf16 tiles loaded by 16-byte buffer-load-to-LDS instructions
+    into a ring of STAGES LDS stages (no VGPR staging); B keeps its
+    n-contiguous layout and is read with the transposing LDS read.  Each tile
+    is offered with 2 stages and with the deepest ring (3 or 4) that fits.
+  * "reg": loads staged through VGPRs into a 2-stage LDS ring (fp32; fp16/bf16
+    operands that are not 16-byte aligned; a few fp16/bf16 tiles for operands
+    whose byte extents exceed 32-bit buffer offsets).
+
 Feasible range (the paper prunes candidates whose use of a hardware level is
 "extremely low or high" without giving thresholds; the thresholds below are
 this library's reading):
   * L1: accumulator registers Mw*Nw/64 in [4, 128] of the 512 per lane, so
     staging, fragments and addresses fit without spilling; aspect <= 4.
   * L2: 4 wavefronts per workgroup (one per SIMD of the CU), or 8 for tiles of
-    at least 128 x 128; LDS for a 2-stage ring <= 160 KiB; every thread moves
-    at least one 16-byte vector of A and of B per K step and at most 32 (<= 128
-    staging VGPRs); the K step reads at least 128 contiguous bytes per row (two
-    64-byte segments); aspect of the workgroup tile <= 8.
+    at least 128 x 128; LDS for a 2-stage ring <= 160 KiB; the K step reads at
+    least 128 contiguous bytes per row (two 64-byte segments); aspect of the
+    workgroup tile <= 8.  DMA tiles: A and B split into whole 1 KiB wave
+    transfers per K step.  Register-staged tiles: every thread moves at least
+    one 16-byte vector of A and of B per K step and at most 32 (<= 128 staging
+    VGPRs).
   * L0 per L1 link: the 32 x 32 MFMA when both wavefront dims are multiples of
     32 and at least 64 (half the fragment loads per FLOP of the 16 x 16 shape),
     else the 16 x 16 MFMA.  The paper takes this decision by profiling L0
@@ -47,6 +59,7 @@ GFX950 = {
     },
 }
 DT_CODE = {"f32": 0, "f16": 1, "bf16": 2}
+LDS_RESERVE = 1024   # the split-K arrival flag and alignment share the CU's LDS
 ELEM_BYTES = {"f32": 4, "f16": 2, "bf16": 2}
 
 
@@ -96,7 +109,28 @@ def lds_bytes(dtype, mb, nb, kb):
     return 2 * stage
 
 
-def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw):
+def lds_bytes_dma(mb, nb, kb, stages):
+    return stages * (mb * kb + kb * nb) * 2
+
+
+def dma_stage_options(mb, nb, kb, wm, wn, mi, vec, hw):
+    """Pipeline depths offered for a DMA tile: 2 and the deepest of 3..4 that
+    fits the LDS and the 6-bit vmcnt of the waits."""
+    nwave = wm * wn
+    lane = 16 if vec else 2
+    wave_bytes = 64 * lane
+    a_bytes, b_bytes = mb * kb * 2, kb * nb * 2
+    if a_bytes % (wave_bytes * nwave) or b_bytes % (wave_bytes * nwave):
+        return []
+    lps = a_bytes // (wave_bytes * nwave) + b_bytes // (wave_bytes * nwave)
+    ok = [st for st in (2, 3, 4)
+          if lds_bytes_dma(mb, nb, kb, st) <= hw["lds_bytes"] - LDS_RESERVE and (st - 2) * lps <= 63]
+    if not ok:
+        return []
+    return sorted({ok[0], ok[-1]})
+
+
+def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw, family):
     eb = ELEM_BYTES[dtype]
     nt = wm * wn * hw["wave"]
     ve = 16 // eb
@@ -109,7 +143,15 @@ def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw):
         return False
     if kb * eb < 128:
         return False
-    if lds_bytes(dtype, mb, nb, kb) > hw["lds_bytes"]:
+    # K chunk of one fragment load
+    kch = (32 if mi == 16 else 16) if eb == 2 else (16 if mi == 16 else 8)
+    if kb % kch:
+        return False
+    if family == "dma":
+        # direct-to-LDS loads: a 2-stage ring of vector DMA must fit
+        return eb == 2 and bool(dma_stage_options(mb, nb, kb, wm, wn, mi, 1, hw))
+    # register-staged loads
+    if lds_bytes(dtype, mb, nb, kb) > hw["lds_bytes"] - LDS_RESERVE:
         return False
     a_vec = mb * kb // ve
     b_vec = nb * kb // ve
@@ -119,30 +161,22 @@ def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw):
         return False
     if a_vec // nt + b_vec // nt > 32:
         return False
-    # K chunk of one fragment load
-    kch = (32 if mi == 16 else 16) if eb == 2 else (16 if mi == 16 else 8)
-    if kb % kch:
-        return False
     if eb == 2:
         # B is staged in blocks of BK rows x 8 columns (BK in {8, 4, 2})
-        ok = False
-        for bk in (8, 4, 2):
-            blocks = (kb // bk) * (nb // 8)
-            if blocks >= nt and blocks % nt == 0:
-                ok = True
-                break
-        if not ok:
+        if not any((kb // bk) * (nb // 8) >= nt and (kb // bk) * (nb // 8) % nt == 0 for bk in (8, 4, 2)):
             return False
     return True
 
 
-def generate_candidates_for_layer(level, dtype, hw=GFX950):
+def generate_candidates_for_layer(level, dtype, hw=GFX950, family=None):
     """Algorithm 2: returns (cands, link) for `level`; link maps a candidate
     to the list of lower-level candidates it is an integer multiple of."""
     hw = get_hardware_info(level, hw)
     if level == 0:
         return filter_by_isa(init_cands_l0(hw), dtype, hw), {}
-    prev, _ = generate_candidates_for_layer(level - 1, dtype, hw)
+    if family is None:
+        family = "dma" if ELEM_BYTES[dtype] == 2 else "reg"
+    prev, _ = generate_candidates_for_layer(level - 1, dtype, hw, family)
     cands, link = [], {}
     if level == 1:
         init = init_cands_l1(hw)
@@ -154,7 +188,7 @@ def generate_candidates_for_layer(level, dtype, hw=GFX950):
                 link[c].append(p)
         return cands, link
     if level == 2:
-        l1_links = generate_candidates_for_layer(1, dtype, hw)[1]
+        l1_links = generate_candidates_for_layer(1, dtype, hw, family)[1]
         kbs = (64, 128, 256) if ELEM_BYTES[dtype] == 2 else (32, 64)
         for (mw, nw) in prev:
             for (wm, wn) in WAVE_GRIDS:
@@ -165,7 +199,7 @@ def generate_candidates_for_layer(level, dtype, hw=GFX950):
                         if mi != want or kb % l0[2]:
                             continue
                         c = (wm * mw, wn * nw, kb, wm, wn, mi)
-                        if not feasible_l2(dtype, *c, hw):
+                        if not feasible_l2(dtype, *c, hw, family):
                             continue
                         if c not in link:
                             cands.append(c)
@@ -175,20 +209,39 @@ def generate_candidates_for_layer(level, dtype, hw=GFX950):
     raise ValueError("gfx950 GEMM has levels 0..2")
 
 
-def registry(hw=GFX950):
-    """All workgroup-level candidates of every dtype, with the load variant.
+# fp16/bf16 register-staged vector-load tiles kept for operands whose byte
+# extents exceed 32-bit buffer offsets
+REG_FALLBACK_16 = [(32, 32, 128, 2, 2, 16), (64, 64, 64, 2, 2, 16), (128, 128, 64, 2, 2, 32)]
 
-    Each candidate is compiled twice: with 16-byte vector loads (operands whose
-    row strides and base addresses are 16-byte aligned) and with element-wise
-    loads (any alignment)."""
+
+def _entry(dtype, family, stages, c, vec, hw):
+    mb, nb, kb, wm, wn, mi = c
+    lds = lds_bytes_dma(mb, nb, kb, stages) if family == "dma" else lds_bytes(dtype, mb, nb, kb)
+    return dict(dtype=dtype, dt=DT_CODE[dtype], family=family, stages=stages, mb=mb, nb=nb, kb=kb, wm=wm,
+                wn=wn, mi=mi, vec=vec, threads=wm * wn * hw["wave"], lds=lds)
+
+
+def registry(hw=GFX950):
+    """All workgroup-level candidates that are compiled into the library.
+
+    fp16/bf16: direct-to-LDS tiles with 16-byte loads (aligned operands), each
+    with a 2-stage and with its deepest ring; register-staged tiles with
+    element-wise loads (any alignment; a 2-byte buffer-to-LDS load fills a
+    whole dword of LDS, so unaligned rows cannot be DMA'd densely); and a few
+    register-staged vector tiles for very large operands.
+    fp32: register-staged tiles, vector and element-wise."""
     out = []
-    for dtype in ("f16", "bf16", "f32"):
-        cands, link = generate_candidates_for_layer(2, dtype, hw)
-        for (mb, nb, kb, wm, wn, mi) in cands:
-            for vec in (1, 0):
-                out.append(dict(dtype=dtype, dt=DT_CODE[dtype], mb=mb, nb=nb, kb=kb, wm=wm, wn=wn,
-                                mi=mi, vec=vec, threads=wm * wn * hw["wave"],
-                                lds=lds_bytes(dtype, mb, nb, kb)))
+    for dtype in ("f16", "bf16"):
+        for c in generate_candidates_for_layer(2, dtype, hw, "dma")[0]:
+            for st in dma_stage_options(*c, 1, hw):
+                out.append(_entry(dtype, "dma", st, c, 1, hw))
+        for c in generate_candidates_for_layer(2, dtype, hw, "reg")[0]:
+            out.append(_entry(dtype, "reg", 2, c, 0, hw))
+        for c in REG_FALLBACK_16:
+            out.append(_entry(dtype, "reg", 2, c, 1, hw))
+    for c in generate_candidates_for_layer(2, "f32", hw, "reg")[0]:
+        for vec in (1, 0):
+            out.append(_entry("f32", "reg", 2, c, vec, hw))
     for i, e in enumerate(out):
         e["id"] = i
     return out

@@ -1,0 +1,238 @@
+// Direct-to-LDS family for fp16/bf16 (gfx950).
+//
+// Level 1 (workgroup) loads its A and B tiles with buffer loads that write
+// LDS directly (no VGPR staging, no VALU), into a ring of STAGES LDS stages,
+// so up to STAGES-1 K steps are in flight while the MFMAs consume the oldest.
+// Out-of-range rows, columns and K tails are given an out-of-range buffer
+// offset: the hardware returns zeros for them, which land in LDS as padding.
+// Each lane moves one 16-byte chunk, so rows must be 16-byte aligned (K and N
+// multiples of 8, aligned bases); other operands use the register-staged
+// family (a 2-byte buffer-to-LDS load fills a whole LDS dword per lane, which
+// cannot build a dense 16-bit tile).
+//
+// LDS layouts (dense, 16-byte chunks XOR-swizzled against bank conflicts):
+//   As[m][k]  Mb x Kb, k contiguous   (chunk c of row m stored at c ^ swzA(m))
+//   Bs[k][n]  Kb x Nb, n contiguous   (chunk c of row k stored at c ^ swzB(k))
+// B stays in its natural n-contiguous layout; the MFMA fragments of B are
+// read with the transposing LDS read: in each 16-lane group, source lane s
+// points at Bs[k0 + s/4][n0 + 4*(s%4)], and output lane j receives
+// Bs[k0 + e][n0 + j] for e = 0..3 — four consecutive k of column j.
+#pragma once
+#include "gemm_kernel.h"
+
+namespace vxk {
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+// LDS addresses stay in address space 3 from the __shared__ object onwards:
+// the compiler's wait tracking for LDS DMA needs to see which object each
+// DMA and each read touches, and a detour through generic pointers hides it.
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+
+template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_>
+struct DCfg {
+    static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_, STAGES = ST_;
+    static constexpr bool VEC = VEC_;
+    static constexpr bool H = true;
+    static constexpr int EB = 2;
+    static constexpr int NWAVE = WM * WN, NT = NWAVE * 64;
+    static constexpr int MW = MB / WM, NW = NB / WN;
+    static constexpr int FM = MW / MI, FN = NW / MI;
+    static constexpr int ACC = MI == 16 ? 4 : 16;
+    static constexpr int KI = MI == 16 ? 32 : 16;
+    static constexpr int A_BYTES = MB * KB * 2, B_BYTES = KB * NB * 2;
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;   // one object per stage
+    static constexpr int CPA = KB / 8, CPB = NB / 8;       // 16-byte chunks per row
+    static constexpr int SWA = CPA < 16 ? CPA : 16;        // A swizzle period (rows)
+    static constexpr int LANE_BYTES = 16;                  // bytes one lane moves per DMA instruction
+    static constexpr int WAVE_BYTES = 64 * LANE_BYTES;
+    static constexpr int A_IPW = A_BYTES / WAVE_BYTES / NWAVE;   // DMA instructions per wave per K step
+    static constexpr int B_IPW = B_BYTES / WAVE_BYTES / NWAVE;
+    static constexpr int LPS = A_IPW + B_IPW;
+
+    static_assert(VEC, "direct-to-LDS loads move 16-byte chunks");
+    static_assert(MB % WM == 0 && NB % WN == 0 && MW % MI == 0 && NW % MI == 0, "tile hierarchy");
+    static_assert(KB % KI == 0 && KB % 8 == 0 && NB % 8 == 0, "K step and chunking");
+    static_assert(A_IPW >= 1 && A_IPW * WAVE_BYTES * NWAVE == A_BYTES, "A DMA must split evenly over waves");
+    static_assert(B_IPW >= 1 && B_IPW * WAVE_BYTES * NWAVE == B_BYTES, "B DMA must split evenly over waves");
+    static_assert(STAGES >= 2 && STAGES <= 4, "pipeline depth");
+    static_assert((STAGES - 2) * LPS <= 63, "vmcnt range");
+    static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
+};
+
+__device__ __forceinline__ int swz_a(int r, int period) { return r & (period - 1); }
+template <int CPB>
+__device__ __forceinline__ int swz_b(int k) { return (2 * (k & 3)) & (CPB - 1); }
+
+// s_waitcnt vmcnt(n) for a compile-time n (expcnt and lgkmcnt left at max).
+template <int N>
+__device__ __forceinline__ void wait_vm()
+{
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+constexpr unsigned kOOB = 0x80000000u;    // buffer offset beyond every resource's range
+
+// One buffer-load-to-LDS instruction: lane i's LANE bytes from the buffer at
+// byte offset voff land at LDS address dst + i*LANE (dst is wave-uniform and
+// goes through M0, set in the same statement).  Issued as inline assembly so
+// that the compiler does not add its own conservative waits for LDS DMA
+// before every LDS read; the pipeline's explicit vmcnt waits order the DMA
+// against the reads of each stage instead.  No compiler-managed value lives
+// in M0 in these kernels (no LDS DMA builtins, no indirect register indexing).
+// Raw buffer resource (stride 0) for a wave-uniform base address: offsets at
+// or beyond num_records read as zero.  Every dword is made scalar explicitly.
+__device__ __forceinline__ u32x4 buffer_rsrc(const void* base, unsigned num_records)
+{
+    const uint64_t a = (uint64_t)base;
+    u32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((unsigned)a);
+    r[1] = __builtin_amdgcn_readfirstlane((unsigned)(a >> 32) & 0xffffu);
+    r[2] = num_records;
+    r[3] = 0x00020000u;
+    return r;
+}
+
+template <int LANE>
+__device__ __forceinline__ void dma_lds(const u32x4& r, lds_char* dst, unsigned voff)
+{
+    static_assert(LANE == 16, "16-byte chunks");
+    const unsigned m0v = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)dst);
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m0v), "v"(voff), "s"(r)
+                 : "memory");
+}
+
+template <class C>
+struct DmaTile {
+    // Issues the DMA of the K step starting at k0 into LDS stage `stage`.
+    __device__ __forceinline__ static void issue(lds_char* stage, const char* Apanel, const char* Bbatch, int k0, int kend,
+                                                 int Mrel, int n0, int N, int K, int wave, int lane)
+    {
+        // A: rows of the workgroup's panel; the resource starts at column k0
+        const u32x4 ra = buffer_rsrc(Apanel + (int64_t)k0 * 2, kOOB);
+        const int kv = kend - k0;   // valid columns from k0
+#pragma unroll
+        for (int i = 0; i < C::A_IPW; ++i) {
+            const int instr = wave * C::A_IPW + i;
+            lds_char* dst = stage + instr * C::WAVE_BYTES;
+            const int slot = instr * 64 + lane;                  // chunk index in the stage
+            const int r = slot / C::CPA, c = (slot % C::CPA) ^ swz_a(r, C::SWA);
+            const bool ok = r < Mrel && c * 8 < kv;
+            dma_lds<C::LANE_BYTES>(ra, dst, ok ? (unsigned)((r * K + c * 8) * 2) : kOOB);
+        }
+        // B: rows k0.. of the batch's B, columns from n0
+        const u32x4 rb = buffer_rsrc(Bbatch + ((int64_t)k0 * N + n0) * 2, kOOB);
+        const int nv = N - n0;      // valid columns from n0
+#pragma unroll
+        for (int i = 0; i < C::B_IPW; ++i) {
+            const int instr = wave * C::B_IPW + i;
+            lds_char* dst = stage + C::A_BYTES + instr * C::WAVE_BYTES;
+            const int slot = instr * 64 + lane;
+            const int k = slot / C::CPB, c = (slot % C::CPB) ^ swz_b<C::CPB>(k);
+            const bool ok = k < kv && c * 8 < nv;
+            dma_lds<C::LANE_BYTES>(rb, dst, ok ? (unsigned)((k * N + c * 8) * 2) : kOOB);
+        }
+    }
+};
+
+// Level 0 over one LDS stage.
+template <class C>
+__device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm0, int wn0, int lane)
+{
+    lds_char* As = stage;
+    lds_char* Bs = stage + C::A_BYTES;
+    const int li = lane % C::MI, lg = lane / C::MI;
+    const int s = lane & 15, grp = lane >> 4;
+    // transposing-read coordinates of this lane (see the header comment)
+    const int tr_n = (C::MI == 16 ? 0 : 16 * (grp & 1)) + 4 * (s & 3);
+    const int tr_k = (C::MI == 16 ? 8 * grp : 8 * (grp >> 1)) + (s >> 2);
+#pragma unroll
+    for (int kk = 0; kk < C::KB / C::KI; ++kk) {
+        u32x4 fa[C::FM], fb[C::FN];
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) {
+            const int m = wm0 + fm * C::MI + li;
+            const int c = (kk * (C::KI / 8) + lg) ^ swz_a(m, C::SWA);
+            fa[fm] = *(lds_u32x4*)(As + m * (C::KB * 2) + c * 16);
+        }
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn) {
+            const int n = wn0 + fn * C::MI + tr_n;
+            const int k1 = kk * C::KI + tr_k, k2 = k1 + 4;
+            lds_char* p1 = Bs + k1 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k1)) << 4) + (n & 7) * 2;
+            lds_char* p2 = Bs + k2 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k2)) << 4) + (n & 7) * 2;
+            const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p1);
+            const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p2);
+            const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+            fb[fn] = u32x4{l2[0], l2[1], h2[0], h2[1]};
+        }
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm) {
+                if constexpr (C::MI == 16)
+                    mfma16<C::DT, 16>(fb[fn], fa[fm], acc.v[fn][fm]);
+                else
+                    mfma32<C::DT>(fb[fn], fa[fm], acc.v[fn][fm]);
+            }
+    }
+}
+
+template <class C>
+__device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& p)
+{
+    // One LDS object per stage: distinct objects let the compiler see that a
+    // DMA into one stage never aliases the reads of another, so it leaves the
+    // loads in flight and the pipeline waits only where wait_steps says.
+    constexpr int SB = C::STAGE_BYTES;
+    __shared__ __attribute__((aligned(1024))) char st0[SB];
+    __shared__ __attribute__((aligned(1024))) char st1[SB];
+    __shared__ __attribute__((aligned(1024))) char st2[C::STAGES > 2 ? SB : 16];
+    __shared__ __attribute__((aligned(1024))) char st3[C::STAGES > 3 ? SB : 16];
+#define VX_STAGE(j) ((lds_char*)((j) == 0 ? st0 : (j) == 1 ? st1 : (j) == 2 ? st2 : st3))
+
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const GridPos g = grid_pos<C::MB, C::NB, C::KB>(p);
+
+    const char* Apanel = (const char*)p.A + ((int64_t)g.b * p.sA + (int64_t)g.m0 * p.K) * 2;
+    const char* Bbatch = (const char*)p.B + (int64_t)g.b * p.sB * 2;
+    const int Mrel = p.M - g.m0;
+    const int wm0 = (wave % C::WM) * C::MW, wn0 = (wave / C::WM) * C::NW;
+
+    Acc<C> acc;
+    acc_zero<C>(acc);
+
+    // Every DMA is issued unconditionally: a step beyond the slice gets only
+    // out-of-range offsets (zero fill, no memory traffic).  Without branches
+    // around the DMAs the number in flight is the same at every wait, and the
+    // compiler's own wait tracking stays exact across the loop.
+    // prologue: the first STAGES-1 K steps, step s into stage s
+#pragma unroll
+    for (int s = 0; s < C::STAGES - 1; ++s)
+        DmaTile<C>::issue(VX_STAGE(s), Apanel, Bbatch, g.kbeg + s * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
+    // main loop, unrolled by STAGES so that every stage index is a constant
+    for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
+#pragma unroll
+        for (int j = 0; j < C::STAGES; ++j) {
+            const int it = it0 + j;
+            if (it >= g.nk)
+                break;
+            wait_vm<(C::STAGES - 2) * C::LPS>();   // step `it` has landed (this wave's part)
+            __builtin_amdgcn_s_barrier();          // ... and every wave's; stage it-1 is free
+            DmaTile<C>::issue(VX_STAGE((j + C::STAGES - 1) % C::STAGES), Apanel, Bbatch,
+                              g.kbeg + (it + C::STAGES - 1) * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
+            dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane);
+        }
+    }
+    wait_vm<0>();   // drain the zero-fill DMAs before LDS is released
+#undef VX_STAGE
+    finish<C>(p, acc, g, t, lane, wm0, wn0);
+}
+
+}  // namespace vxk

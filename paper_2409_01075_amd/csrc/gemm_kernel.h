@@ -75,7 +75,7 @@ struct Cfg {
     static_assert(AV >= 1 && AV * VE * NT == MB * KB, "A tile must split evenly over threads");
     static_assert(BV >= 1 && (H ? BV * 8 : BV * 4) * NT == NB * KB, "B tile must split evenly over threads");
     static_assert(!H || !VEC || (BBLK >= 1 && BBLK * NT * BK * 8 == KB * NB), "B blocks must split evenly");
-    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one CU");
+    static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
 };
 
 __device__ __forceinline__ unsigned lo16(unsigned w) { return w & 0xffffu; }
@@ -374,47 +374,47 @@ __device__ __forceinline__ void acc_coord(int lane, int g, int& dm, int& dn)
     }
 }
 
-// ------------------------------------------------------- level 2 + level 1 --
-template <class C>
-__device__ __forceinline__ void gemm_body(const VxGemmArgs& p)
+// ---------------------------------------------------------- level 2 -------
+// Grid level: the parallel loop over (batch, K slice, tile) of one launch.
+struct GridPos {
+    int b, z, tm, tn, m0, n0, kbeg, kend, nk, tiles;
+};
+
+template <int MB, int NB, int KB>
+__device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
 {
-    __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
-
-    const int t = threadIdx.x;
-    const int lane = t & 63, wave = t >> 6;
-
-    // Grid level: workgroups are dispatched round-robin over the XCDs; remap
-    // the linear id so that each XCD receives a contiguous range of logical
-    // tiles (neighbouring tiles share A or B panels in that XCD's L2).
+    // Workgroups are dispatched round-robin over the XCDs; remap the linear id
+    // so that each XCD receives a contiguous range of logical tiles
+    // (neighbouring tiles share A or B panels in that XCD's L2).
     const int G = gridDim.x, w = blockIdx.x;
     const int nx = p.num_xcd;
     const int xcd = w % nx, q = G / nx, rem = G % nx;
     const int wl = xcd * q + (xcd < rem ? xcd : rem) + w / nx;
 
-    const int tiles = p.tiles_m * p.tiles_n;
-    const int tile = wl % tiles;
-    const int bz = wl / tiles;
-    const int z = bz % p.split, b = bz / p.split;
+    GridPos g;
+    g.tiles = p.tiles_m * p.tiles_n;
+    const int tile = wl % g.tiles;
+    const int bz = wl / g.tiles;
+    g.z = bz % p.split;
+    g.b = bz / p.split;
     // grouped order: group_m tile rows are walked column by column
     const int per_group = p.group_m * p.tiles_n;
     const int grp = tile / per_group;
     const int first_m = grp * p.group_m;
     const int gm = min(p.group_m, p.tiles_m - first_m);
-    const int tm = first_m + (tile % per_group) % gm;
-    const int tn = (tile % per_group) / gm;
+    g.tm = first_m + (tile % per_group) % gm;
+    g.tn = (tile % per_group) / gm;
+    g.m0 = g.tm * MB;
+    g.n0 = g.tn * NB;
+    g.kbeg = g.z * p.k_per_split;
+    g.kend = min(p.K, g.kbeg + p.k_per_split);
+    g.nk = g.kend > g.kbeg ? (g.kend - g.kbeg + KB - 1) / KB : 0;
+    return g;
+}
 
-    const int m0 = tm * C::MB, n0 = tn * C::NB;
-    const int kbeg = z * p.k_per_split;
-    const int kend = min(p.K, kbeg + p.k_per_split);
-    const int nk = kend > kbeg ? (kend - kbeg + C::KB - 1) / C::KB : 0;
-
-    const char* Ab = (const char*)p.A + ((int64_t)b * p.sA + (int64_t)m0 * p.K) * C::EB;
-    const char* Bb = (const char*)p.B + (int64_t)b * p.sB * C::EB;
-    const int Mrel = p.M - m0;
-
-    const int wm0 = (wave % C::WM) * C::MW, wn0 = (wave / C::WM) * C::NW;
-
-    Acc<C> acc;
+template <class C>
+__device__ __forceinline__ void acc_zero(Acc<C>& acc)
+{
 #pragma unroll
     for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
@@ -422,35 +422,24 @@ __device__ __forceinline__ void gemm_body(const VxGemmArgs& p)
 #pragma unroll
             for (int e = 0; e < C::ACC; ++e)
                 acc.v[fn][fm][e] = 0.0f;
+}
 
-    Tile<C> tl;
-    if (nk > 0) {
-        tl.load(Ab, Bb, 0, n0, kbeg, kend, Mrel, p.N, p.K, t);
-        tl.store(smem, t);
-    }
-    __syncthreads();
-    for (int it = 0; it < nk; ++it) {
-        char* cur = smem + (it & 1) * C::STAGE_BYTES;
-        if (it + 1 < nk)
-            tl.load(Ab, Bb, 0, n0, kbeg + (it + 1) * C::KB, kend, Mrel, p.N, p.K, t);
-        compute_step<C>(cur, acc, wm0, wn0, lane);
-        if (it + 1 < nk)
-            tl.store(smem + ((it + 1) & 1) * C::STAGE_BYTES, t);
-        __syncthreads();
-    }
-
-    char* Cb = (char*)p.C + (int64_t)b * p.sC * C::EB;
-    constexpr int NG = C::ACC / 4;
-
+// ------------------------------------------------------------ Store_Func ---
+// Split-K reduction (when the launch splits K) and the epilogue: fp32
+// accumulators -> output type (round to nearest even) -> predicated stores.
+template <class C>
+__device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const GridPos& g, int t, int lane,
+                                       int wm0, int wn0)
+{
     if (p.split > 1) {
         // Split-K: publish this slice's fp32 partial tile, then the last slice
         // to arrive sums all slices in order 0..split-1 and writes C.
         // The partials travel through device-coherent (agent-scope) stores and
         // loads, so no workgroup has to write back or invalidate a whole L2.
         constexpr int PER = C::FN * C::FM * C::ACC;       // floats per thread
-        const int64_t tile_id = (int64_t)b * tiles + tm * p.tiles_n + tn;
+        const int64_t tile_id = (int64_t)g.b * g.tiles + g.tm * p.tiles_n + g.tn;
         float* wt = p.ws + tile_id * (int64_t)p.split * (PER * C::NT);
-        float* mine = wt + (int64_t)z * (PER * C::NT);
+        float* mine = wt + (int64_t)g.z * (PER * C::NT);
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
@@ -475,34 +464,74 @@ __device__ __forceinline__ void gemm_body(const VxGemmArgs& p)
 #pragma unroll
                 for (int e = 0; e < C::ACC; ++e) {
                     const int64_t o = ((fn * C::FM + fm) * C::ACC + e) * C::NT + t;
-                    float s = z == 0 ? acc.v[fn][fm][e]
-                                     : __hip_atomic_load(wt + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    float s = g.z == 0 ? acc.v[fn][fm][e]
+                                       : __hip_atomic_load(wt + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     for (int zz = 1; zz < p.split; ++zz)
-                        s += zz == z ? acc.v[fn][fm][e]
-                                     : __hip_atomic_load(wt + (int64_t)zz * (PER * C::NT) + o, __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT);
+                        s += zz == g.z ? acc.v[fn][fm][e]
+                                       : __hip_atomic_load(wt + (int64_t)zz * (PER * C::NT) + o, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT);
                     acc.v[fn][fm][e] = s;
                 }
         if (t == 0)
             __hip_atomic_store(&p.tickets[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 
+    char* Cb = (char*)p.C + (int64_t)g.b * p.sC * C::EB;
+    constexpr int NG = C::ACC / 4;
     const bool cvec = p.c_vec != 0;
 #pragma unroll
     for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm)
 #pragma unroll
-            for (int g = 0; g < NG; ++g) {
+            for (int gi = 0; gi < NG; ++gi) {
                 int dm, dn;
-                acc_coord<C::MI>(lane, g, dm, dn);
-                const int m = m0 + wm0 + fm * C::MI + dm;
-                const int n = n0 + wn0 + fn * C::MI + dn;
+                acc_coord<C::MI>(lane, gi, dm, dn);
+                const int m = g.m0 + wm0 + fm * C::MI + dm;
+                const int n = g.n0 + wn0 + fn * C::MI + dn;
                 if (m < p.M)
                     store4<C::DT>(Cb, (int64_t)m * p.N + n, n, p.N, cvec,
-                                  acc.v[fn][fm][4 * g], acc.v[fn][fm][4 * g + 1],
-                                  acc.v[fn][fm][4 * g + 2], acc.v[fn][fm][4 * g + 3]);
+                                  acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1],
+                                  acc.v[fn][fm][4 * gi + 2], acc.v[fn][fm][4 * gi + 3]);
             }
+}
+
+// ------------------------------------------------- register-staged family --
+// Level 1 with loads staged through VGPRs (any dtype; 16-bit B is transposed
+// in registers on its way into LDS).
+template <class C>
+__device__ __forceinline__ void gemm_body(const VxGemmArgs& p)
+{
+    __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
+
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const GridPos g = grid_pos<C::MB, C::NB, C::KB>(p);
+
+    const char* Ab = (const char*)p.A + ((int64_t)g.b * p.sA + (int64_t)g.m0 * p.K) * C::EB;
+    const char* Bb = (const char*)p.B + (int64_t)g.b * p.sB * C::EB;
+    const int Mrel = p.M - g.m0;
+    const int wm0 = (wave % C::WM) * C::MW, wn0 = (wave / C::WM) * C::NW;
+
+    Acc<C> acc;
+    acc_zero<C>(acc);
+
+    Tile<C> tl;
+    if (g.nk > 0) {
+        tl.load(Ab, Bb, 0, g.n0, g.kbeg, g.kend, Mrel, p.N, p.K, t);
+        tl.store(smem, t);
+    }
+    __syncthreads();
+    for (int it = 0; it < g.nk; ++it) {
+        char* cur = smem + (it & 1) * C::STAGE_BYTES;
+        if (it + 1 < g.nk)
+            tl.load(Ab, Bb, 0, g.n0, g.kbeg + (it + 1) * C::KB, g.kend, Mrel, p.N, p.K, t);
+        compute_step<C>(cur, acc, wm0, wn0, lane);
+        if (it + 1 < g.nk)
+            tl.store(smem + ((it + 1) & 1) * C::STAGE_BYTES, t);
+        __syncthreads();
+    }
+    finish<C>(p, acc, g, t, lane, wm0, wn0);
 }
 
 }  // namespace vxk

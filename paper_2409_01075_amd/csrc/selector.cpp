@@ -11,6 +11,10 @@
 //                        T_Load  = load latency + tile bytes / L2->CU share,
 //                        Cost_0  = level-0 cost, T_Store = epilogue bytes
 //                        (+ split-K partial traffic and arrival counter)   Eq. 2
+//                        With an LDS ring of S stages, S-1 K steps are in
+//                        flight: after the first step, a new step is ready
+//                        every max(transfer, T_Load / (S-1)); Eq. 2 is this
+//                        with S = 2.
 //   level 2 (grid)       parallel loop over tiles x slices x batch:
 //                        F = ceil(workgroups / (CUs x resident WGs per CU)) Eq. 3
 //                        Cost_2 = F x T_temporal(level 1)                  Eq. 4
@@ -77,6 +81,12 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
         if ((double)tiles * split * k.mb * k.nb * 4.0 > (double)lim.ws_bytes)
             return -1.0;
     }
+    if (k.family == 1) {
+        // direct-to-LDS kernels address each K step with 32-bit buffer offsets:
+        // Mb rows of A (Mb*K elements) and Kb rows of B (Kb*N elements)
+        if ((double)k.mb * sh.K * eb >= 2147483648.0 || (double)k.kb * sh.N * eb >= 2147483648.0)
+            return -1.0;
+    }
     if (k_per_split)
         *k_per_split = (int)kps;
 
@@ -109,13 +119,21 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     // Level 1: the K loop of one workgroup (Eq. 2 over n_k K steps).
     const double bw_wg = hw.l2_bytes_clk_cu * hw.clock_ghz / per_cu;                // B/ns
     const double load_factor = k.vec ? 1.0 : 4.0;   // element-wise loads: 8x the instructions
-    const double t_load = hw.mem_latency_ns + (double)(k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
+    const double xfer = (double)(k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
+    const double t_load = hw.mem_latency_ns + xfer;
     double t_store = (double)k.mb * k.nb * eb / bw_wg;
     if (split > 1) {
         const double part = (double)k.mb * k.nb * 4.0 / bw_wg;
         t_store += part + hw.atomic_latency_ns + hw.mem_latency_ns + (double)(split - 1) * part;
     }
-    const double t1 = vx_cost_temporal(t_load, nk, cost0, t_store);
+    const int depth = std::max(1, k.stages - 1);
+    double t1;
+    if (depth == 1 || nk <= 1) {
+        t1 = vx_cost_temporal(t_load, nk, cost0, t_store);
+    } else {
+        const double t_issue = std::max(xfer, t_load / depth);
+        t1 = t_load + (double)(nk - 1) * std::max(t_issue, cost0) + cost0 + t_store;
+    }
 
     // Level 2 (Eq. 4), dispatch constant, compulsory-traffic floor.
     const double cost2 = (double)F * t1;
