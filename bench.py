@@ -48,7 +48,39 @@ def _parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--detail", default=None, help="write per-M results as JSON to this path")
+    ap.add_argument("--rot-mib", type=int, default=512,
+                    help="bytes of rotating operand copies per timing window (MiB)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run one plain device-to-device copy of this size (MiB): a "
+                         "kernel of known traffic for calibrating memory counters under a profiler")
     return ap.parse_args()
+
+
+def _kernel_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm_kernel.h", "gemm_dma.h", "vx_args.h", "candidates.py"):
+        with open(os.path.join(ROOT, "paper_2409_01075_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _profiled_traffic(kernel_name):
+    """HBM traffic per launch from the committed counter summary, if it was
+    taken on the current kernel sources for this kernel; else None."""
+    path = os.path.join(ROOT, "profiles", "sweep_f16_traffic.txt")
+    try:
+        kv = {}
+        with open(path) as f:
+            for ln in f:
+                if ln.strip() and not ln.startswith("#"):
+                    k, _, v = ln.strip().partition(" ")
+                    kv[k] = v
+    except OSError:
+        return None
+    if kv.get("kernel") != kernel_name or kv.get("kernel_source_sha") != _kernel_source_sha():
+        return None
+    return float(kv["traffic_bytes_per_launch"])
 
 
 def _cpu_threads():
@@ -127,7 +159,7 @@ def main():
                 raise RuntimeError("vx_gemm M=%d: %s" % (M, vx.STATUS.get(st, st)))
 
     # rotating pools: R_M copies of M's operands, R_M * set bytes >= 512 MiB
-    rot_bytes = 512 * 2 ** 20
+    rot_bytes = args.rot_mib * 2 ** 20
     reps = {M: max(8, -(-rot_bytes // ((M * K + K * N + M * N) * 2))) for M in ms}
     pool_a = torch.empty(max(reps[M] * M * K for M in ms), dtype=torch.float16, device=dev)
     pool_b = torch.empty(max(reps[M] * K * N for M in ms), dtype=torch.float16, device=dev)
@@ -195,6 +227,16 @@ def main():
         torch.cuda.synchronize()
         pass_ms.append(e0.elapsed_time(e1))
 
+    if args.copy_mib > 0:
+        n = args.copy_mib * 2 ** 20 // 2
+        src = torch.empty(n, dtype=torch.float16, device=dev)
+        dst = torch.empty(n, dtype=torch.float16, device=dev)
+        src.fill_(1.0)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     med = np.median(np.array(per_step), axis=0)        # ms per call, per M
     flops = np.array([2.0 * M * N * K for M in ms])
     tflops = flops / (med * 1e-3) / 1e12
@@ -215,7 +257,7 @@ def main():
     kinfo = vx.vx_registry_get(kid)
     achieved = d["bytes"] / d["t"] / 1e9          # GB/s
     roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                "frac": achieved / HBM_PEAK_GBPS, "traffic": _profiled_traffic("vxk_%d" % kid),
                 "kernel": "vxk_%d" % kid,
                 "tile": [kinfo.mb, kinfo.nb, kinfo.kb, kinfo.wm, kinfo.wn, kinfo.mfma_m],
                 "launches_per_step": d["n"], "avg_us": d["t"] / d["n"] * 1e6,
