@@ -42,6 +42,11 @@ N_SWEEP, K_SWEEP = 768, 768
 def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "encoder", "attention", "llm", "single"],
+                    help="sweep (default, the headline metric) or one of the other GEMM sets")
+    ap.add_argument("--trials", type=int, default=None, help="trials of a GEMM set (default: the full set)")
+    ap.add_argument("--compare-torch", action="store_true",
+                    help="also time torch.matmul on each GEMM of a set (context only)")
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--m-max", type=int, default=512, help="sweep M = 1..m_max")
@@ -116,12 +121,178 @@ def _cpu_baseline(ms, budget_s):
                       % ("{%d..%d}" % (done[0], done[-1]), len(done))}
 
 
+def _set_jobs(name, trials):
+    """(label, batch, M, N, K, dtype, make) for every GEMM of a set; make(dev)
+    returns seeded device operands (A, B) of the set's distributions."""
+    from paper_2409_01075_amd import inputs as I
+    import torch
+    bf = torch.bfloat16
+    jobs = []
+    if name == "single":
+        def mk(dev):
+            A, B = I.single_f32(0)
+            return torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
+        return [("fp32 77x96x80", 1, 77, 96, 80, 0, mk)]
+    if name == "encoder":
+        for t in range(64 if trials is None else trials):
+            M = I.encoder_shape(t)
+            for gi, (K, N) in enumerate(I.ENCODER_SHAPES):
+                def mk(dev, t=t, gi=gi, M=M, K=K, N=N):
+                    return (I.device_normal((M, K), 1.0, 1000 * t + 2 * gi, dev, bf),
+                            I.device_normal((K, N), 0.02, 1000 * t + 2 * gi + 1, dev, bf))
+                jobs.append(("t%d G%d (%d,%d)x(%d,%d)" % (t, gi + 1, M, K, K, N), 1, M, N, K, 2, mk))
+    elif name == "llm":
+        for t in range(48 if trials is None else trials):
+            M = I.llm_M(t)
+            for gi, (K, N) in enumerate(I.LLM_SHAPES):
+                def mk(dev, t=t, gi=gi, M=M, K=K, N=N):
+                    return (I.device_normal((M, K), 1.0, 1000 * t + 2 * gi, dev, bf),
+                            I.device_normal((K, N), 0.02, 1000 * t + 2 * gi + 1, dev, bf))
+                jobs.append(("t%d H%d (%d,%d)x(%d,%d)" % (t, gi + 1, M, K, K, N), 1, M, N, K, 2, mk))
+    elif name == "attention":
+        b, d = I.ATTN_BATCH, I.ATTN_HEAD
+        for t in range(32 if trials is None else trials):
+            L = I.attention_L(t)
+            def mk_s(dev, t=t, L=L):
+                return (I.device_normal((b, L, d), 1.0, 1000 * t, dev, bf),
+                        I.device_normal((b, d, L), 1.0, 1000 * t + 1, dev, bf))
+            def mk_o(dev, t=t, L=L):
+                return (I.device_softmax_rows((b, L, L), 1000 * t + 2, dev, bf),
+                        I.device_normal((b, L, d), 1.0, 1000 * t + 3, dev, bf))
+            jobs.append(("t%d S L=%d" % (t, L), b, L, L, d, 2, mk_s))
+            jobs.append(("t%d O L=%d" % (t, L), b, L, d, L, 2, mk_o))
+    return jobs
+
+
+def run_set(args):
+    """Times every GEMM of a set over rotating HBM-resident copies and reports
+    TFLOP/s and the fraction of each shape's roofline."""
+    import numpy as np
+    import torch
+    from paper_2409_01075_amd import vx
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = vx.lib()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    jobs = _set_jobs(args.workload, args.trials)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    torch.cuda._sleep(1000000)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    cycles_per_ms = 1e6 / max(e0.elapsed_time(e1), 1e-3)
+    results = []
+    for (label, b, M, N, K, dt, mk) in jobs:
+        eb = 4 if dt == 0 else 2
+        A, B = mk(dev)
+        set_bytes = b * (M * K + K * N + M * N) * eb
+        R = int(min(max(2, -(-args.rot_mib * 2 ** 20 // set_bytes)), 4096))
+        pa = A.reshape(1, -1).expand(R, -1).contiguous()
+        pb = B.reshape(1, -1).expand(R, -1).contiguous()
+        pc = torch.empty((R, b * M * N), dtype=A.dtype, device=dev)
+        sa, sb, sc = b * M * K * eb, b * K * N * eb, b * M * N * eb
+        a0, b0, c0 = pa.data_ptr(), pb.data_ptr(), pc.data_ptr()
+
+        def call(r):
+            if b == 1:
+                return L.vx_gemm(M, N, K, dt, a0 + r * sa, b0 + r * sb, c0 + r * sc, sp)
+            return L.vx_gemm_batched(b, M, N, K, dt, a0 + r * sa, M * K, b0 + r * sb, K * N, c0 + r * sc,
+                                     M * N, sp)
+        st = call(0)
+        if st != 0:
+            raise RuntimeError("%s: %s" % (label, vx.STATUS.get(st, st)))
+        torch.cuda.synchronize()
+        times = []
+        n_calls = max(R, 8)
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(int(cycles_per_ms * 0.3))
+            e0.record(stream)
+            for i in range(n_calls):
+                call(i % R)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / n_calls * 1e-3)
+        t = float(np.median(times))
+        plan = vx.vx_plan_query(b, M, N, K, dt, M * K, K * N, M * N)
+        flops = 2.0 * b * M * N * K
+        bytes_min = float(set_bytes)
+        t_mfma = flops / (MFMA_PEAK_TFLOPS[dt] * 1e12)
+        t_hbm = bytes_min / (HBM_PEAK_GBPS * 1e9)
+        r = {"label": label, "batch": b, "M": M, "N": N, "K": K, "us": t * 1e6, "tflops": flops / t / 1e12,
+             "gbps": bytes_min / t / 1e9, "bound": "mfma" if t_mfma >= t_hbm else "hbm",
+             "roof_frac": max(t_mfma, t_hbm) / t, "kernel": plan.kernel_id, "split": plan.split_k,
+             "tile": [plan.kernel.mb, plan.kernel.nb, plan.kernel.kb, plan.kernel.stages]}
+        if args.compare_torch:
+            At = A.reshape(b, M, K) if b > 1 else A
+            Bt = B.reshape(b, K, N) if b > 1 else B
+            torch.matmul(At, Bt)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(8):
+                torch.matmul(At, Bt)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            r["torch_us"] = e0.elapsed_time(e1) / 8 * 1e3
+        results.append(r)
+        print("%-34s %9.1f us %8.1f TFLOP/s %7.0f GB/s  %s %5.1f%% of roof  kid %d split %d %s%s"
+              % (label, r["us"], r["tflops"], r["gbps"], r["bound"], 100 * r["roof_frac"], r["kernel"],
+                 r["split"], r["tile"], ("  torch %.1f us" % r["torch_us"]) if "torch_us" in r else ""),
+              file=sys.stderr, flush=True)
+        del pa, pb, pc, A, B
+
+    def geo(v):
+        v = [x for x in v if x > 0]
+        return float(np.exp(np.mean(np.log(v)))) if v else None
+    hbm = [r for r in results if r["bound"] == "hbm"]
+    mf = [r for r in results if r["bound"] == "mfma"]
+    by_kernel = {}
+    for r in results:
+        by_kernel.setdefault(r["kernel"], []).append(r)
+    kid = max(by_kernel, key=lambda k: sum(r["us"] for r in by_kernel[k]))
+    dom = by_kernel[kid]
+    dom_bound = max(set(r["bound"] for r in dom), key=lambda x: sum(r["us"] for r in dom if r["bound"] == x))
+    dom_t = sum(r["us"] for r in dom) * 1e-6
+    if dom_bound == "hbm":
+        ach = sum(r["batch"] * (r["M"] * r["K"] + r["K"] * r["N"] + r["M"] * r["N"]) * 2.0 for r in dom) / dom_t / 1e9
+        roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBPS}
+    else:
+        ach = sum(2.0 * r["batch"] * r["M"] * r["N"] * r["K"] for r in dom) / dom_t / 1e12
+        roof = {"bound": "mfma", "achieved": ach, "peak": MFMA_PEAK_TFLOPS[2], "unit": "TFLOP/s",
+                "frac": ach / MFMA_PEAK_TFLOPS[2]}
+    roof.update({"traffic": None, "kernel": "vxk_%d" % kid, "launches": len(dom),
+                 "avg_us": dom_t / len(dom) * 1e6})
+    out = {"metric": "GEMM TFLOP/s geomean over dynamic-M sweep; % of MFMA/HBM roofline on 1 GPU",
+           "value": geo([r["tflops"] for r in results]), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": 1, "warmup": 1, "ms_per_step": sum(r["us"] for r in results) / 1e3,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f32" if args.workload == "single" else "bf16", "data": "synthetic (seeded, on device)",
+           "config": {"workload": args.workload, "gemms": len(results)},
+           "roofline": roof,
+           "roof_frac_geomean": geo([r["roof_frac"] for r in results]),
+           "hbm_bound": {"n": len(hbm), "gbps_geomean": geo([r["gbps"] for r in hbm]),
+                         "frac_geomean": geo([r["roof_frac"] for r in hbm])},
+           "mfma_bound": {"n": len(mf), "tflops_geomean": geo([r["tflops"] for r in mf]),
+                          "frac_geomean": geo([r["roof_frac"] for r in mf])}}
+    if args.compare_torch:
+        out["vs_torch_matmul_geomean"] = geo([r["torch_us"] / r["us"] for r in results])
+    if args.detail:
+        with open(args.detail, "w") as f:
+            json.dump(results, f)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the GEMM path is single-device; "
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.workload != "sweep":
+        run_set(args)
+        return
     import numpy as np
     import torch
     from paper_2409_01075_amd import inputs as I

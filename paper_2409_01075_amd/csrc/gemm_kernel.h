@@ -434,20 +434,31 @@ __device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const G
     if (p.split > 1) {
         // Split-K: publish this slice's fp32 partial tile, then the last slice
         // to arrive sums all slices in order 0..split-1 and writes C.
-        // The partials travel through device-coherent (agent-scope) stores and
-        // loads, so no workgroup has to write back or invalidate a whole L2.
+        // Partials move as 16-byte device-coherent (sc1) buffer stores and
+        // loads, laid out [slice][group of 4 accumulators][thread] so each
+        // wave instruction covers 1 KiB contiguously; no workgroup has to
+        // write back or invalidate a whole L2.
         constexpr int PER = C::FN * C::FM * C::ACC;       // floats per thread
+        constexpr int P4 = PER / 4;
+        constexpr unsigned SLICE_BYTES = (unsigned)PER * C::NT * 4;   // = Mb * Nb * 4
         const int64_t tile_id = (int64_t)g.b * g.tiles + g.tm * p.tiles_n + g.tn;
-        float* wt = p.ws + tile_id * (int64_t)p.split * (PER * C::NT);
-        float* mine = wt + (int64_t)g.z * (PER * C::NT);
+        const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(p.ws + tile_id * (int64_t)p.split * (PER * C::NT)), (short)0, (int)(SLICE_BYTES * p.split),
+            0x00020000);
+        constexpr int SC1 = 16;   // cache policy: device scope
+        const unsigned mine = (unsigned)g.z * SLICE_BYTES;
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm)
 #pragma unroll
-                for (int e = 0; e < C::ACC; ++e)
-                    __hip_atomic_store(&mine[((fn * C::FM + fm) * C::ACC + e) * C::NT + t], acc.v[fn][fm][e],
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                for (int gi = 0; gi < C::ACC / 4; ++gi) {
+                    const int e4 = (fn * C::FM + fm) * (C::ACC / 4) + gi;
+                    const f32x4 part = {acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1], acc.v[fn][fm][4 * gi + 2],
+                                        acc.v[fn][fm][4 * gi + 3]};
+                    const u32x4 v = __builtin_bit_cast(u32x4, part);
+                    __builtin_amdgcn_raw_buffer_store_b128(v, rw, mine + (unsigned)(e4 * C::NT + t) * 16, 0, SC1);
+                }
         // every store of the partial tile has completed before the arrival is counted
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
@@ -457,20 +468,28 @@ __device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const G
         __syncthreads();
         if (arrived != (unsigned)(p.split - 1))
             return;
+        static_assert(PER % 4 == 0, "accumulators come in groups of 4");
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm)
 #pragma unroll
-                for (int e = 0; e < C::ACC; ++e) {
-                    const int64_t o = ((fn * C::FM + fm) * C::ACC + e) * C::NT + t;
-                    float s = g.z == 0 ? acc.v[fn][fm][e]
-                                       : __hip_atomic_load(wt + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    for (int zz = 1; zz < p.split; ++zz)
-                        s += zz == g.z ? acc.v[fn][fm][e]
-                                       : __hip_atomic_load(wt + (int64_t)zz * (PER * C::NT) + o, __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT);
-                    acc.v[fn][fm][e] = s;
+                for (int gi = 0; gi < C::ACC / 4; ++gi) {
+                    const int e4 = (fn * C::FM + fm) * (C::ACC / 4) + gi;
+                    const unsigned off = (unsigned)(e4 * C::NT + t) * 16;
+                    f32x4 own = {acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1], acc.v[fn][fm][4 * gi + 2],
+                                 acc.v[fn][fm][4 * gi + 3]};
+                    f32x4 sum = g.z == 0 ? own
+                                         : __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, SC1));
+                    for (int zz = 1; zz < p.split; ++zz) {
+                        const f32x4 part = zz == g.z ? own
+                                                     : __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                                                     rw, zz * SLICE_BYTES + off, 0, SC1));
+                        sum += part;
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc.v[fn][fm][4 * gi + e] = sum[e];
                 }
         if (t == 0)
             __hip_atomic_store(&p.tickets[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -142,6 +142,27 @@ def llm_trial(t, gemms=(0, 1, 2)):
     return M, out
 
 
+def device_normal(shape, std, seed, device, dtype):
+    """Seeded N(0, std) values drawn on the device (for timing runs at full
+    workload sizes, where host generation would dominate the run time)."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    t = torch.empty(shape, dtype=torch.float32, device=device)
+    t.normal_(0.0, std, generator=gen)
+    return t.to(dtype)
+
+
+def device_softmax_rows(shape, seed, device, dtype):
+    """Seeded row softmax of N(0, 1) logits, drawn on the device (timing runs)."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    z = torch.empty(shape, dtype=torch.float32, device=device)
+    z.normal_(0.0, 1.0, generator=gen)
+    return torch.softmax(z, dim=-1).to(dtype)
+
+
 def small_int(g, shape, dtype, lo, hi):
     """Integers drawn uniformly from [lo, hi] (inclusive), stored exactly."""
     return to_storage(g.integers(lo, hi + 1, size=shape).astype(np.float64), dtype)
