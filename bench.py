@@ -42,9 +42,13 @@ N_SWEEP, K_SWEEP = 768, 768
 def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "encoder", "attention", "llm", "single"],
+    ap.add_argument("--workload", default="sweep",
+                    choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single"],
                     help="sweep (default, the headline metric) or one of the other GEMM sets")
     ap.add_argument("--trials", type=int, default=None, help="trials of a GEMM set (default: the full set)")
+    ap.add_argument("--study", action="store_true",
+                    help="selector quality study: time every feasible (kernel, split) plan of each GEMM "
+                         "of the set and compare the analytical pick with the best")
     ap.add_argument("--compare-torch", action="store_true",
                     help="also time torch.matmul on each GEMM of a set (context only)")
     ap.add_argument("--steps", type=int, default=10)
@@ -128,6 +132,14 @@ def _set_jobs(name, trials):
     import torch
     bf = torch.bfloat16
     jobs = []
+    if name == "sweep-sample":
+        for M in (1, 4, 16, 33, 64, 100, 128, 200, 256, 320, 384, 448, 512):
+            def mk(dev, M=M):
+                A, B = I.sweep_f16(M)
+                return (torch.from_numpy(A.view("int16")).to(dev).view(torch.float16),
+                        torch.from_numpy(B.view("int16")).to(dev).view(torch.float16))
+            jobs.append(("sweep M=%d" % M, 1, M, 768, 768, 1, mk))
+        return jobs
     if name == "single":
         def mk(dev):
             A, B = I.single_f32(0)
@@ -162,6 +174,99 @@ def _set_jobs(name, trials):
             jobs.append(("t%d S L=%d" % (t, L), b, L, L, d, 2, mk_s))
             jobs.append(("t%d O L=%d" % (t, L), b, L, d, L, 2, mk_o))
     return jobs
+
+
+def _time_calls(call, R, stream, spin_cycles, reps=3):
+    import numpy as np
+    import torch
+    n_calls = max(R, 8)
+    times = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(spin_cycles)
+        e0.record(stream)
+        for i in range(n_calls):
+            call(i % R)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) / n_calls * 1e-3)
+    return float(np.median(times))
+
+
+def run_study(args):
+    """Selector quality: for each GEMM, the analytical plan's time against the
+    best time over every feasible (kernel, split) plan of the registry."""
+    import numpy as np
+    import torch
+    from paper_2409_01075_amd import vx
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = vx.lib()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    torch.cuda._sleep(1000000)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    spin = int(1e6 / max(e0.elapsed_time(e1), 1e-3) * 0.3)
+    reg = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]
+    rows = []
+    for (label, b, M, N, K, dt, mk) in _set_jobs(args.workload, args.trials):
+        eb = 4 if dt == 0 else 2
+        A, B = mk(dev)
+        set_bytes = b * (M * K + K * N + M * N) * eb
+        R = int(min(max(2, -(-args.rot_mib * 2 ** 20 // set_bytes)), 4096))
+        pa = A.reshape(1, -1).expand(R, -1).contiguous()
+        pb = B.reshape(1, -1).expand(R, -1).contiguous()
+        pc = torch.empty((R, b * M * N), dtype=A.dtype, device=dev)
+        sa, sb, sc = b * M * K * eb, b * K * N * eb, b * M * N * eb
+        a0, b0, c0 = pa.data_ptr(), pb.data_ptr(), pc.data_ptr()
+
+        def call(r):
+            st = L.vx_gemm_batched(b, M, N, K, dt, a0 + r * sa, M * K, b0 + r * sb, K * N, c0 + r * sc, M * N, sp)
+            if st != 0:
+                raise RuntimeError("%s: %s" % (label, vx.STATUS.get(st, st)))
+        vx.vx_force_plan(-1, 0)
+        plan = vx.vx_plan_query(b, M, N, K, dt, M * K, K * N, M * N)
+        call(0)
+        t_pick = _time_calls(call, R, stream, spin)
+        vec_ok = plan.kernel.vec
+        best = (t_pick, plan.kernel_id, plan.split_k)
+        n_tried = 0
+        for k in reg:
+            if k.dtype != dt or not k.enabled or (k.vec and not vec_ok):
+                continue
+            for split in (1, 2, 4, 8):
+                st, _ = vx.vx_plan_cost(b, M, N, K, dt, k.id, split, vec_ok)
+                if st != 0:
+                    continue
+                vx.vx_force_plan(k.id, split)
+                try:
+                    call(0)
+                    t = _time_calls(call, R, stream, spin, reps=1)
+                finally:
+                    vx.vx_force_plan(-1, 0)
+                n_tried += 1
+                if t < best[0]:
+                    best = (t, k.id, split)
+        kb = vx.vx_registry_get(best[1])
+        row = {"label": label, "M": M, "N": N, "K": K, "batch": b, "pick_us": t_pick * 1e6,
+               "pick": [plan.kernel_id, plan.split_k], "best_us": best[0] * 1e6, "best": [best[1], best[2]],
+               "best_tile": [kb.mb, kb.nb, kb.kb, kb.wm, kb.wn, kb.stages], "frac_of_best": best[0] / t_pick,
+               "tried": n_tried}
+        rows.append(row)
+        print("%-30s pick %8.1f us %s  best %8.1f us %s %s  -> %.1f%% of best (%d plans)"
+              % (label, row["pick_us"], row["pick"], row["best_us"], row["best"], row["best_tile"],
+                 100 * row["frac_of_best"], n_tried), file=sys.stderr, flush=True)
+        del pa, pb, pc, A, B
+    geo = float(np.exp(np.mean(np.log([r["frac_of_best"] for r in rows]))))
+    out = {"study": args.workload, "gemms": len(rows), "selector_frac_of_best_geomean": geo,
+           "selector_frac_of_best_min": min(r["frac_of_best"] for r in rows)}
+    if args.detail:
+        with open(args.detail, "w") as f:
+            json.dump(rows, f)
+    print(json.dumps(out), flush=True)
 
 
 def run_set(args):
@@ -290,6 +395,9 @@ def main():
         print("bench.py measures one GPU only: the GEMM path is single-device; "
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.study:
+        run_study(args)
+        return
     if args.workload != "sweep":
         run_set(args)
         return

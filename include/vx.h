@@ -155,9 +155,34 @@ vx_status vx_get_hwinfo(vx_hwinfo* out);
  * NULL restores the real device.  Does not change which kernels exist. */
 vx_status vx_set_hwinfo_override(const vx_hwinfo* hw);
 
+/*
+ * Offline calibration of the kernels' low levels — the empirical part of the
+ * hybrid analyzer (Section 5.2): per kernel, the measured time of one
+ * workgroup K step and the fixed per-call cost, with the device fully and
+ * lightly loaded, taken once per device on synthetic shapes derived from the
+ * kernel's own tile and the CU count (never from application shapes).  The
+ * table is written by paper_2409_01075_amd/calibrate.py and is used only if
+ * it was measured on this exact kernel set (vx_registry_hash).  The library
+ * tries the default file (calib_<arch>.txt next to the library) at its first
+ * plan; without it the selector is purely analytical.
+ *
+ * vx_calibration_load: path NULL = the default file; *n_loaded = kernels read.
+ * Returns VX_ERR_INVALID_ARG if the file is missing, malformed or was taken on
+ * another kernel set; a failed explicit path keeps the table in use, a failed
+ * default (NULL) leaves no table in use.  vx_calibration_enable(0) returns to the analytical
+ * model (ablation); vx_calibration_active reports whether it is in use.
+ */
+vx_status vx_calibration_load(const char* path, int* n_loaded);
+vx_status vx_calibration_enable(int enable);
+int vx_calibration_active(void);
+const char* vx_registry_hash(void);
+
 /* Registry introspection. */
 int vx_registry_count(void);
 vx_status vx_registry_get(int id, vx_kernel_info* out);
+/* Workgroups of a kernel resident per CU on the current device description
+ * (the tighter of its LDS and register budgets). */
+vx_status vx_kernel_occupancy(int kernel_id, int* wgs_per_cu);
 
 /*
  * Pin every following call to one kernel and split-K factor (kernel_id < 0

@@ -1,9 +1,13 @@
 // C ABI of the runtime-shaped GEMM library: argument checks, hardware
 // description, plan cache, split-K workspace, launch (Section 6.2: analytical
 // selection at run time, then the grid is computed from the runtime shape).
+#include <dlfcn.h>
+#include <stdio.h>
 #include <string.h>
 
 #include <atomic>
+#include <string>
+#include <vector>
 #include <map>
 #include <mutex>
 #include <unordered_map>
@@ -19,6 +23,11 @@ constexpr size_t kDefaultPartials = 64ull * 1024 * 1024;   // fp32 split-K parti
 constexpr int kMaxDevices = 64;
 
 std::mutex g_mu;
+std::mutex& g_calib_try_mu()
+{
+    static std::mutex m;
+    return m;
+}
 bool g_override_set = false;
 vx_hwinfo g_override;
 bool g_hw_valid[kMaxDevices];
@@ -57,6 +66,89 @@ struct Workspace {
     bool owned = false;
 };
 std::map<std::pair<int, void*>, Workspace> g_ws;
+
+// ---- offline calibration of the kernels (empirical low levels) ------------
+std::vector<VxCalib> g_calib;
+std::vector<char> g_calib_ok;
+double g_calib_launch_ns = 0.0;
+std::atomic<bool> g_calib_loaded{false};
+std::atomic<bool> g_calib_enabled{true};
+std::atomic<bool> g_calib_tried{false};
+
+std::string default_calib_path(const char* arch)
+{
+    Dl_info info;
+    std::string dir = ".";
+    if (dladdr((void*)&vx_version, &info) && info.dli_fname) {
+        dir = info.dli_fname;
+        size_t slash = dir.rfind('/');
+        dir = slash == std::string::npos ? "." : dir.substr(0, slash);
+    }
+    return dir + "/calib_" + arch + ".txt";
+}
+
+// Parses a calibration table; accepts it only for this exact kernel set.
+int load_calib_file(const char* path, const char* arch)
+{
+    FILE* f = fopen(path, "r");
+    if (!f)
+        return -1;
+    int n = 0;
+    vxi_registry(&n);
+    std::vector<VxCalib> cal(n);
+    std::vector<char> ok(n, 0);
+    double launch = 0.0;
+    bool hash_ok = false, arch_ok = arch == nullptr;
+    int loaded = 0;
+    char line[512];
+    while (fgets(line, sizeof line, f)) {
+        char key[64], val[128];
+        if (line[0] == '#' || sscanf(line, "%63s", key) != 1)
+            continue;
+        if (!strcmp(key, "registry_hash") && sscanf(line, "%*s %127s", val) == 1)
+            hash_ok = !strcmp(val, vxi_registry_hash());
+        else if (!strcmp(key, "arch") && sscanf(line, "%*s %127s", val) == 1)
+            arch_ok = arch == nullptr || !strcmp(val, arch);
+        else if (!strcmp(key, "launch_ns"))
+            sscanf(line, "%*s %lf", &launch);
+        else if (!strcmp(key, "kernel")) {
+            int id;
+            VxCalib c;
+            c.split_a = c.split_b = -1.0;
+            if (sscanf(line, "%*s %d %lf %lf %lf %lf %lf %lf %lf", &id, &c.step_full, &c.fix_full, &c.step_light,
+                       &c.fix_light, &c.load_light, &c.split_a, &c.split_b) >= 6 &&
+                id >= 0 && id < n && c.step_full > 0.0 && c.step_light > 0.0 && c.load_light > 0.0) {
+                cal[id] = c;
+                ok[id] = 1;
+                ++loaded;
+            }
+        }
+    }
+    fclose(f);
+    if (!hash_ok || !arch_ok || loaded == 0)
+        return -2;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_calib.swap(cal);
+        g_calib_ok.swap(ok);
+        g_calib_launch_ns = launch;
+        g_plans.clear();
+    }
+    g_calib_loaded.store(true);
+    g_epoch.fetch_add(1);
+    return loaded;
+}
+
+void ensure_calib(const vx_hwinfo& hw)
+{
+    if (g_calib_tried.load())
+        return;
+    std::lock_guard<std::mutex> lk(g_calib_try_mu());
+    if (g_calib_tried.load())
+        return;
+    load_calib_file(default_calib_path(hw.arch).c_str(), hw.arch);
+    g_calib_tried.store(true);
+}
 
 int elem_bytes(int dt) { return dt == VX_F32 ? 4 : 2; }
 
@@ -115,6 +207,7 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
     vx_status st = hwinfo_for(dev, &hw);
     if (st != VX_OK)
         return st;
+    ensure_calib(hw);
     VxLimits lim;
     lim.ws_bytes = ws_bytes;
     lim.max_tickets = ws_bytes ? (int64_t)(kTicketBytes / 4) : 0;
@@ -266,7 +359,80 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
 
 }  // namespace
 
+const VxCalib* vxi_calib(int kernel_id)
+{
+    if (!g_calib_loaded.load() || !g_calib_enabled.load())
+        return nullptr;
+    if (kernel_id < 0 || kernel_id >= (int)g_calib_ok.size() || !g_calib_ok[kernel_id])
+        return nullptr;
+    return &g_calib[kernel_id];
+}
+
+double vxi_calib_launch_ns(const vx_hwinfo& hw)
+{
+    if (g_calib_loaded.load() && g_calib_enabled.load() && g_calib_launch_ns > 0.0)
+        return g_calib_launch_ns;
+    return hw.launch_ns;
+}
+
 extern "C" {
+
+vx_status vx_calibration_load(const char* path, int* n_loaded)
+{
+    vx_hwinfo hw;
+    const char* arch = nullptr;
+    int dev = 0;
+    if (current_device(&dev) == VX_OK && hwinfo_for(dev, &hw) == VX_OK)
+        arch = hw.arch;
+    std::string p = path ? std::string(path) : default_calib_path(arch ? arch : "gfx950");
+    g_calib_tried.store(true);
+    const int n = load_calib_file(p.c_str(), path ? nullptr : arch);
+    if (n <= 0 && !path) {
+        // no usable default table: the selector is purely analytical
+        g_calib_loaded.store(false);
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_plans.clear();
+        g_epoch.fetch_add(1);
+    }
+    if (n_loaded)
+        *n_loaded = n > 0 ? n : 0;
+    return n > 0 ? VX_OK : VX_ERR_INVALID_ARG;
+}
+
+vx_status vx_calibration_enable(int enable)
+{
+    g_calib_enabled.store(enable != 0);
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_plans.clear();
+    g_epoch.fetch_add(1);
+    return VX_OK;
+}
+
+int vx_calibration_active(void)
+{
+    return (g_calib_loaded.load() && g_calib_enabled.load()) ? 1 : 0;
+}
+
+const char* vx_registry_hash(void) { return vxi_registry_hash(); }
+
+vx_status vx_kernel_occupancy(int kernel_id, int* wgs_per_cu)
+{
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    if (!wgs_per_cu || kernel_id < 0 || kernel_id >= n)
+        return VX_ERR_INVALID_ARG;
+    int dev = 0;
+    vx_status st = current_device(&dev);
+    if (st != VX_OK)
+        return st;
+    vx_hwinfo hw;
+    st = hwinfo_for(dev, &hw);
+    if (st != VX_OK)
+        return st;
+    *wgs_per_cu = vxi_occupancy(hw, reg[kernel_id].info);
+    return VX_OK;
+}
+
 
 vx_status vx_gemm(int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A, const void* B, void* C,
                   void* stream)

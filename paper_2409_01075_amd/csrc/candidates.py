@@ -27,8 +27,9 @@ workgroup level):
 Feasible range (the paper prunes candidates whose use of a hardware level is
 "extremely low or high" without giving thresholds; the thresholds below are
 this library's reading):
-  * L1: accumulator registers Mw*Nw/64 in [4, 128] of the 512 per lane, so
-    staging, fragments and addresses fit without spilling; aspect <= 4.
+  * L1: accumulator registers Mw*Nw/64 in [4, 128] of the 512 per lane for
+    register-staged tiles (staging, fragments and addresses must fit beside
+    them), [4, 256] for direct-to-LDS tiles (no staging registers); aspect <= 4.
   * L2: 4 wavefronts per workgroup (one per SIMD of the CU), or 8 for tiles of
     at least 128 x 128; LDS for a 2-stage ring <= 160 KiB; the K step reads at
     least 128 contiguous bytes per row (two 64-byte segments); aspect of the
@@ -80,12 +81,16 @@ def filter_by_isa(cands, dtype, hw):
 
 
 # ------------------------------------------------------------------ L1 -----
-def init_cands_l1(hw):
+def init_cands_l1(hw, family="reg"):
+    # accumulator budget: register-staged tiles keep up to 128 VGPRs for the
+    # staging registers; direct-to-LDS tiles stage nothing in VGPRs and may
+    # hold 256 fp32 accumulators per lane (the AGPR half of the file)
+    acc_max = 256 if family == "dma" else 128
     out = []
     for mw in (16, 32, 64, 128, 256):
         for nw in (16, 32, 64, 128, 256):
             acc = mw * nw // hw["wave"]
-            if 4 <= acc <= 128 and max(mw, nw) <= 4 * min(mw, nw):
+            if 4 <= acc <= acc_max and max(mw, nw) <= 4 * min(mw, nw):
                 out.append((mw, nw))
     return out
 
@@ -179,7 +184,7 @@ def generate_candidates_for_layer(level, dtype, hw=GFX950, family=None):
     prev, _ = generate_candidates_for_layer(level - 1, dtype, hw, family)
     cands, link = [], {}
     if level == 1:
-        init = init_cands_l1(hw)
+        init = init_cands_l1(hw, family)
         for p in prev:
             for c in multiples_l1(p, init):
                 if c not in link:

@@ -20,6 +20,13 @@
 //                        Cost_2 = F x T_temporal(level 1)                  Eq. 4
 // The call's cost adds the dispatch constant and is floored by the
 // compulsory HBM traffic at peak bandwidth.  The plan is the argmin (Eq. 1).
+//
+// Hybrid analyzer (Section 5.2): when an offline calibration of the kernels
+// is loaded, the low levels are empirical — each kernel's measured time per
+// workgroup K step and fixed cost (with the device fully loaded and lightly
+// loaded) replace the analytical level-0/level-1 estimate — and the grid
+// level stays analytical: F - 1 full waves of workgroups plus a last, partial
+// wave whose per-step time is interpolated by its load (Eq. 3, Eq. 4).
 #include <math.h>
 
 #include <algorithm>
@@ -51,6 +58,18 @@ int vxi_group_m(int64_t tiles_m, int64_t tiles_n)
 
 // Splits considered for K (the grid-level share of the reduction loop).
 static const int kSplits[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32};
+
+int vxi_occupancy(const vx_hwinfo& hw, const vx_kernel_info& k)
+{
+    // Resident workgroups per CU: the tighter of the LDS and register budgets.
+    const int waves = k.wm * k.wn;
+    const int regs = ((k.vgprs + 7) / 8) * 8 + ((k.agprs + 7) / 8) * 8;
+    int waves_simd = regs > 0 ? hw.vgprs_per_lane / regs : hw.max_waves_per_simd;
+    waves_simd = std::max(1, std::min(waves_simd, hw.max_waves_per_simd));
+    const int by_regs = std::max(1, waves_simd * hw.simd_per_cu / waves);
+    const int by_lds = std::max(1, hw.lds_bytes_per_cu / std::max(1, k.lds_bytes));
+    return std::min(by_regs, by_lds);
+}
 
 double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k, int split,
                 const VxLimits& lim, int* k_per_split)
@@ -90,14 +109,8 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     if (k_per_split)
         *k_per_split = (int)kps;
 
-    // Resident workgroups per CU: the tighter of the LDS and register budgets.
     const int waves = k.wm * k.wn;
-    const int regs = ((k.vgprs + 7) / 8) * 8 + ((k.agprs + 7) / 8) * 8;
-    int waves_simd = regs > 0 ? hw.vgprs_per_lane / regs : hw.max_waves_per_simd;
-    waves_simd = std::max(1, std::min(waves_simd, hw.max_waves_per_simd));
-    const int by_regs = std::max(1, waves_simd * hw.simd_per_cu / waves);
-    const int by_lds = std::max(1, hw.lds_bytes_per_cu / std::max(1, k.lds_bytes));
-    const int occ = std::min(by_regs, by_lds);
+    const int occ = vxi_occupancy(hw, k);
     const int64_t slots = (int64_t)hw.num_cu * occ;
 
     // Level 2: wave quantisation over the device (Eq. 3).
@@ -135,10 +148,29 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
         t1 = t_load + (double)(nk - 1) * std::max(t_issue, cost0) + cost0 + t_store;
     }
 
-    // Level 2 (Eq. 4), dispatch constant, compulsory-traffic floor.
-    const double cost2 = (double)F * t1;
     const double bytes_min = (double)sh.batch * ((double)sh.M * sh.K + (double)sh.K * sh.N + (double)sh.M * sh.N) * eb;
     const double floor_ns = bytes_min / hw.hbm_gbps;
+
+    const VxCalib* cb = vxi_calib(k.id);
+    if (cb) {
+        // empirical low levels, analytical grid level
+        double t_split = t_store - (double)k.mb * k.nb * eb / bw_wg;   // split-K epilogue, analytical
+        if (split > 1 && cb->split_a >= 0.0 && cb->split_b >= 0.0)
+            t_split = cb->split_a + cb->split_b * (double)(split - 1);      // ... or measured
+        const double load_last = (double)(units - (F - 1) * slots) / (double)slots;
+        auto at_load = [&](double full, double light) {
+            if (load_last <= cb->load_light || cb->load_light >= 1.0)
+                return light;
+            return light + (full - light) * (load_last - cb->load_light) / (1.0 - cb->load_light);
+        };
+        const double wave_full = cb->fix_full + (double)nk * cb->step_full;
+        const double wave_last = at_load(cb->fix_full, cb->fix_light) + (double)nk * at_load(cb->step_full, cb->step_light);
+        const double cost2 = (double)(F - 1) * wave_full + wave_last + t_split;
+        return vxi_calib_launch_ns(hw) + std::max(cost2, floor_ns);
+    }
+
+    // Level 2 (Eq. 4), dispatch constant, compulsory-traffic floor.
+    const double cost2 = (double)F * t1;
     return hw.launch_ns + std::max(cost2, floor_ns);
 }
 

@@ -14,6 +14,20 @@ struct VxKernelEntry {
 
 // The generated registry (one entry per compiled workgroup-level candidate).
 const VxKernelEntry* vxi_registry(int* count);
+// Identifies the compiled kernel set (candidates + kernel sources).
+const char* vxi_registry_hash(void);
+
+// Offline per-kernel measurements (the empirical low levels of the hybrid
+// analyzer): time of one workgroup K step and fixed per-call cost, with the
+// whole device busy ("full") and at light load, all in ns.
+struct VxCalib {
+    double step_full, fix_full, step_light, fix_light, load_light;
+    double split_a, split_b;   // split-K epilogue: split_a + split_b * (slices - 1); < 0 if not measured
+};
+// Calibration of a kernel, or nullptr when none is loaded / it is disabled.
+const VxCalib* vxi_calib(int kernel_id);
+// Dispatch constant: the calibrated launch floor when loaded, else hw.launch_ns.
+double vxi_calib_launch_ns(const vx_hwinfo& hw);
 
 // Device description from hipDeviceProp_t plus the per-architecture table.
 // Returns 0 on success.
@@ -31,6 +45,9 @@ struct VxLimits {
     size_t ws_bytes;        // split-K partials capacity
     int64_t max_tickets;    // arrival counters available
 };
+
+// Resident workgroups per CU of kernel k (tighter of LDS and register budgets).
+int vxi_occupancy(const vx_hwinfo& hw, const vx_kernel_info& k);
 
 // Cost (ns) of kernel k with split s on shape sh; < 0 if infeasible.  On
 // success also returns the K extent per slice.

@@ -83,6 +83,16 @@ def lib():
     L.vx_force_plan.restype = i32
     L.vx_set_workspace.argtypes = [vp, ctypes.c_size_t, vp]
     L.vx_set_workspace.restype = i32
+    L.vx_calibration_load.argtypes = [ctypes.c_char_p, ctypes.POINTER(i32)]
+    L.vx_calibration_load.restype = i32
+    L.vx_calibration_enable.argtypes = [i32]
+    L.vx_calibration_enable.restype = i32
+    L.vx_calibration_active.argtypes = []
+    L.vx_calibration_active.restype = i32
+    L.vx_kernel_occupancy.argtypes = [i32, ctypes.POINTER(i32)]
+    L.vx_kernel_occupancy.restype = i32
+    L.vx_registry_hash.argtypes = []
+    L.vx_registry_hash.restype = ctypes.c_char_p
     L.vx_status_string.argtypes = [i32]
     L.vx_status_string.restype = ctypes.c_char_p
     L.vx_version.argtypes = []
@@ -153,6 +163,30 @@ def vx_force_plan(kernel_id, split_k=0):
 
 def vx_set_workspace(ptr, nbytes, stream=None):
     return lib().vx_set_workspace(ptr, nbytes, stream)
+
+
+def vx_calibration_load(path=None):
+    n = ctypes.c_int(0)
+    st = lib().vx_calibration_load(None if path is None else path.encode(), ctypes.byref(n))
+    return st, n.value
+
+
+def vx_calibration_enable(enable):
+    return lib().vx_calibration_enable(1 if enable else 0)
+
+
+def vx_calibration_active():
+    return lib().vx_calibration_active()
+
+
+def vx_kernel_occupancy(kernel_id):
+    n = ctypes.c_int(0)
+    _chk(lib().vx_kernel_occupancy(kernel_id, ctypes.byref(n)), "vx_kernel_occupancy")
+    return n.value
+
+
+def vx_registry_hash():
+    return lib().vx_registry_hash().decode()
 
 
 def vx_status_string(s):
