@@ -43,12 +43,15 @@ def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--workload", default="sweep",
-                    choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single"],
+                    choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single", "mixed"],
                     help="sweep (default, the headline metric) or one of the other GEMM sets")
     ap.add_argument("--trials", type=int, default=None, help="trials of a GEMM set (default: the full set)")
     ap.add_argument("--study", action="store_true",
                     help="selector quality study: time every feasible (kernel, split) plan of each GEMM "
-                         "of the set and compare the analytical pick with the best")
+                         "of the set and compare the selector's pick, and the Static1/Static2 hierarchy "
+                         "ablations, with the best")
+    ap.add_argument("--no-calibration", action="store_true",
+                    help="ablation: plan with the purely analytical cost model (ignore the calibration table)")
     ap.add_argument("--compare-torch", action="store_true",
                     help="also time torch.matmul on each GEMM of a set (context only)")
     ap.add_argument("--steps", type=int, default=10)
@@ -65,15 +68,6 @@ def _parse():
     return ap.parse_args()
 
 
-def _kernel_source_sha():
-    import hashlib
-    h = hashlib.sha256()
-    for f in ("gemm_kernel.h", "gemm_dma.h", "vx_args.h", "candidates.py"):
-        with open(os.path.join(ROOT, "paper_2409_01075_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def _profiled_traffic(kernel_name):
     """HBM traffic per launch from the committed counter summary, if it was
     taken on the current kernel sources for this kernel; else None."""
@@ -87,9 +81,15 @@ def _profiled_traffic(kernel_name):
                     kv[k] = v
     except OSError:
         return None
-    if kv.get("kernel") != kernel_name or kv.get("kernel_source_sha") != _kernel_source_sha():
+    from paper_2409_01075_amd import vx
+    if kv.get("kernel") != kernel_name or kv.get("registry_hash") != vx.vx_registry_hash():
         return None
     return float(kv["traffic_bytes_per_launch"])
+
+
+def _selector_kind():
+    from paper_2409_01075_amd import vx
+    return "hybrid (calibrated)" if vx.vx_calibration_active() else "analytical"
 
 
 def _cpu_threads():
@@ -132,6 +132,12 @@ def _set_jobs(name, trials):
     import torch
     bf = torch.bfloat16
     jobs = []
+    if name == "mixed":
+        # the study's whole benchmark: samples of every set, so that a static
+        # strategy has to serve the full range of shapes at once
+        return (_set_jobs("sweep-sample", None) + _set_jobs("llm", 6 if trials is None else trials)
+                + _set_jobs("encoder", 4 if trials is None else trials)
+                + _set_jobs("attention", 3 if trials is None else trials))
     if name == "sweep-sample":
         for M in (1, 4, 16, 33, 64, 100, 128, 200, 256, 320, 384, 448, 512):
             def mk(dev, M=M):
@@ -193,9 +199,55 @@ def _time_calls(call, R, stream, spin_cycles, reps=3):
     return float(np.median(times))
 
 
+def _study_ctx(job, dev, rot_mib, L, sp):
+    """Rotating device copies of one GEMM of a set and a call(r) closure."""
+    import torch
+    from paper_2409_01075_amd import vx
+    label, b, M, N, K, dt, mk = job
+    eb = 4 if dt == 0 else 2
+    A, B = mk(dev)
+    set_bytes = b * (M * K + K * N + M * N) * eb
+    R = int(min(max(2, -(-rot_mib * 2 ** 20 // set_bytes)), 4096))
+    pa = A.reshape(1, -1).expand(R, -1).contiguous()
+    pb = B.reshape(1, -1).expand(R, -1).contiguous()
+    pc = torch.empty((R, b * M * N), dtype=A.dtype, device=dev)
+    del A, B
+    sa, sb, sc = b * M * K * eb, b * K * N * eb, b * M * N * eb
+    a0, b0, c0 = pa.data_ptr(), pb.data_ptr(), pc.data_ptr()
+
+    def call(r):
+        st = L.vx_gemm_batched(b, M, N, K, dt, a0 + r * sa, M * K, b0 + r * sb, K * N, c0 + r * sc, M * N, sp)
+        if st != 0:
+            raise RuntimeError("%s: %s" % (label, vx.STATUS.get(st, st)))
+    return call, R, (pa, pb, pc)
+
+
+def _wave(k):
+    return (k.mb // k.wm, k.nb // k.wn, k.mfma_m)
+
+
+def _most_frequent(items):
+    """Most frequent item; ties go to the one seen first."""
+    counts, first = {}, {}
+    for i, x in enumerate(items):
+        counts[x] = counts.get(x, 0) + 1
+        first.setdefault(x, i)
+    return max(counts, key=lambda x: (counts[x], -first[x]))
+
+
 def run_study(args):
-    """Selector quality: for each GEMM, the analytical plan's time against the
-    best time over every feasible (kernel, split) plan of the registry."""
+    """Selector quality and the hierarchy ablations (Section 7.4).
+
+    Pass 1, per GEMM of the set: the time of the selector's plan and of every
+    feasible (kernel, split in {1, 2, 4, 8}) plan of the registry; the best of
+    them stands in for the per-shape profiled upper bound.
+    Pass 2, per dtype and alignment class of the set: Static1 fixes the
+    wavefront strategy (wavefront tile and MFMA instruction) that is most
+    often optimal over the class's GEMMs and leaves the workgroup tile and the
+    split to the selector; Static2 also fixes the workgroup tile, the one most
+    often optimal among kernels with that wavefront strategy, and leaves only
+    the split (a grid-level choice) to the selector.  Each is reported as a
+    fraction of the best."""
     import numpy as np
     import torch
     from paper_2409_01075_amd import vx
@@ -211,29 +263,20 @@ def run_study(args):
     torch.cuda.synchronize()
     spin = int(1e6 / max(e0.elapsed_time(e1), 1e-3) * 0.3)
     reg = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]
-    rows = []
-    for (label, b, M, N, K, dt, mk) in _set_jobs(args.workload, args.trials):
+    jobs = _set_jobs(args.workload, args.trials)
+    rows, tables = [], []
+    vx.vx_force_plan(-1, 0)
+    vx.vx_fix_wavefront(0, 0, 0)
+    for job in jobs:
+        label, b, M, N, K, dt, mk = job
         eb = 4 if dt == 0 else 2
-        A, B = mk(dev)
-        set_bytes = b * (M * K + K * N + M * N) * eb
-        R = int(min(max(2, -(-args.rot_mib * 2 ** 20 // set_bytes)), 4096))
-        pa = A.reshape(1, -1).expand(R, -1).contiguous()
-        pb = B.reshape(1, -1).expand(R, -1).contiguous()
-        pc = torch.empty((R, b * M * N), dtype=A.dtype, device=dev)
-        sa, sb, sc = b * M * K * eb, b * K * N * eb, b * M * N * eb
-        a0, b0, c0 = pa.data_ptr(), pb.data_ptr(), pc.data_ptr()
-
-        def call(r):
-            st = L.vx_gemm_batched(b, M, N, K, dt, a0 + r * sa, M * K, b0 + r * sb, K * N, c0 + r * sc, M * N, sp)
-            if st != 0:
-                raise RuntimeError("%s: %s" % (label, vx.STATUS.get(st, st)))
-        vx.vx_force_plan(-1, 0)
+        ve = 16 // eb
+        vec_ok = int(K % ve == 0 and N % ve == 0 and (b == 1 or (M * K) % ve == 0))
+        call, R, keep = _study_ctx(job, dev, args.rot_mib, L, sp)
         plan = vx.vx_plan_query(b, M, N, K, dt, M * K, K * N, M * N)
         call(0)
         t_pick = _time_calls(call, R, stream, spin)
-        vec_ok = plan.kernel.vec
-        best = (t_pick, plan.kernel_id, plan.split_k)
-        n_tried = 0
+        table = {}
         for k in reg:
             if k.dtype != dt or not k.enabled or (k.vec and not vec_ok):
                 continue
@@ -244,28 +287,92 @@ def run_study(args):
                 vx.vx_force_plan(k.id, split)
                 try:
                     call(0)
-                    t = _time_calls(call, R, stream, spin, reps=1)
+                    table[(k.id, split)] = _time_calls(call, R, stream, spin, reps=1)
                 finally:
                     vx.vx_force_plan(-1, 0)
-                n_tried += 1
-                if t < best[0]:
-                    best = (t, k.id, split)
-        kb = vx.vx_registry_get(best[1])
-        row = {"label": label, "M": M, "N": N, "K": K, "batch": b, "pick_us": t_pick * 1e6,
-               "pick": [plan.kernel_id, plan.split_k], "best_us": best[0] * 1e6, "best": [best[1], best[2]],
-               "best_tile": [kb.mb, kb.nb, kb.kb, kb.wm, kb.wn, kb.stages], "frac_of_best": best[0] / t_pick,
-               "tried": n_tried}
+        del keep, call
+        pick = (plan.kernel_id, plan.split_k)
+        table[pick] = min(t_pick, table.get(pick, t_pick))
+        bk = min(table, key=table.get)
+        kb = reg[bk[0]]
+        row = {"label": label, "M": M, "N": N, "K": K, "batch": b, "dtype": dt, "vec_ok": vec_ok,
+               "pick_us": t_pick * 1e6, "pick": list(pick), "best_us": table[bk] * 1e6, "best": list(bk),
+               "best_tile": [kb.mb, kb.nb, kb.kb, kb.wm, kb.wn, kb.stages], "best_wave": list(_wave(kb)),
+               "tried": len(table)}
         rows.append(row)
-        print("%-30s pick %8.1f us %s  best %8.1f us %s %s  -> %.1f%% of best (%d plans)"
-              % (label, row["pick_us"], row["pick"], row["best_us"], row["best"], row["best_tile"],
-                 100 * row["frac_of_best"], n_tried), file=sys.stderr, flush=True)
-        del pa, pb, pc, A, B
-    geo = float(np.exp(np.mean(np.log([r["frac_of_best"] for r in rows]))))
-    out = {"study": args.workload, "gemms": len(rows), "selector_frac_of_best_geomean": geo,
-           "selector_frac_of_best_min": min(r["frac_of_best"] for r in rows)}
+        tables.append(table)
+        print("%-30s pick %8.1f us %s  best %8.1f us %s %s  (%d plans)"
+              % (label, row["pick_us"], row["pick"], row["best_us"], row["best"], row["best_tile"], len(table)),
+              file=sys.stderr, flush=True)
+
+    # ---- pass 2: the static ablations, one fixed strategy per (dtype, alignment class)
+    classes = sorted({(r["dtype"], r["vec_ok"]) for r in rows})
+    fixed = {}
+    for c in classes:
+        idx = [i for i, r in enumerate(rows) if (r["dtype"], r["vec_ok"]) == c]
+        s1 = _most_frequent([tuple(rows[i]["best_wave"]) for i in idx])
+        per = []
+        for i in idx:
+            cand = {kp: t for kp, t in tables[i].items() if _wave(reg[kp[0]]) == s1}
+            if cand:
+                per.append(min(cand, key=cand.get)[0])
+        fixed[c] = (s1, _most_frequent(per) if per else None)
+
+    def timed_plan(i, plan):
+        key = (plan.kernel_id, plan.split_k)
+        if key not in tables[i]:
+            call, R, keep = _study_ctx(jobs[i], dev, args.rot_mib, L, sp)
+            vx.vx_force_plan(*key)
+            try:
+                call(0)
+                tables[i][key] = _time_calls(call, R, stream, spin, reps=1)
+            finally:
+                vx.vx_force_plan(-1, 0)
+            del keep, call
+        return key, tables[i][key]
+
+    for i, r in enumerate(rows):
+        label, b, M, N, K, dt, mk = jobs[i]
+        s1, s2 = fixed[(dt, r["vec_ok"])]
+        vx.vx_fix_wavefront(*s1)
+        try:
+            p1 = vx.vx_plan_query(b, M, N, K, dt, M * K, K * N, M * N)
+        finally:
+            vx.vx_fix_wavefront(0, 0, 0)
+        k1, t1 = timed_plan(i, p1)
+        k2, t2 = None, None
+        if s2 is not None:
+            vx.vx_force_plan(s2, 0)
+            try:
+                p2 = vx.vx_plan_query(b, M, N, K, dt, M * K, K * N, M * N)
+            except vx.VxError:
+                p2 = None
+            finally:
+                vx.vx_force_plan(-1, 0)
+            if p2 is not None:
+                k2, t2 = timed_plan(i, p2)
+        best = min(tables[i].values())
+        r.update({"best_us": best * 1e6, "frac_of_best": best / (r["pick_us"] * 1e-6),
+                  "static1": {"wave": list(s1), "plan": list(k1), "us": t1 * 1e6, "frac_of_best": best / t1},
+                  "static2": None if t2 is None else
+                  {"kernel": s2, "plan": list(k2), "us": t2 * 1e6, "frac_of_best": best / t2}})
+        print("%-30s selector %.1f%%  static1 %.1f%% %s  static2 %s of best"
+              % (label, 100 * r["frac_of_best"], 100 * best / t1, list(k1),
+                 "-" if t2 is None else "%.1f%% %s" % (100 * best / t2, list(k2))), file=sys.stderr, flush=True)
+
+    def geo(xs):
+        return float(np.exp(np.mean(np.log(xs)))) if xs else None
+    f0 = [r["frac_of_best"] for r in rows]
+    f1 = [r["static1"]["frac_of_best"] for r in rows]
+    f2 = [r["static2"]["frac_of_best"] for r in rows if r["static2"]]
+    out = {"study": args.workload, "gemms": len(rows), "selector_frac_of_best_geomean": geo(f0),
+           "selector_frac_of_best_min": min(f0), "static1_frac_of_best_geomean": geo(f1),
+           "static2_frac_of_best_geomean": geo(f2), "static2_gemms": len(f2),
+           "fixed": {"dtype%d_vec%d" % c: {"wave": list(v[0]), "kernel": v[1]} for c, v in fixed.items()}}
     if args.detail:
         with open(args.detail, "w") as f:
             json.dump(rows, f)
+    out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
 
 
@@ -386,6 +493,7 @@ def run_set(args):
     if args.detail:
         with open(args.detail, "w") as f:
             json.dump(results, f)
+    out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
 
 
@@ -395,6 +503,9 @@ def main():
         print("bench.py measures one GPU only: the GEMM path is single-device; "
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.no_calibration:
+        from paper_2409_01075_amd import vx
+        vx.vx_calibration_enable(0)
     if args.study:
         run_study(args)
         return
@@ -429,7 +540,7 @@ def main():
     plans = {M: vx.vx_plan_query(1, M, N, K, vx.VX_F16) for M in ms}
     for M in ms:
         if plans[M].kernel.vec == 0:
-            raise RuntimeError("aligned sweep shape M=%d planned with an element-wise kernel" % M)
+            raise RuntimeError("aligned sweep shape M=%d planned with an element-aligned kernel" % M)
 
     def one_pass():
         for (M, a, b, c) in calls:
@@ -569,6 +680,7 @@ def main():
                        "kernel": [plans[M].kernel_id for M in ms], "split": [plans[M].split_k for M in ms],
                        "by_kernel": {str(k): {kk: vv for kk, vv in v.items()} for k, v in by_kernel.items()}},
                       f)
+    out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
 
 

@@ -85,7 +85,7 @@ typedef struct vx_kernel_info {
     int mb, nb, kb;                /* workgroup tile */
     int wm, wn;                    /* wavefront grid; wavefront tile = (mb/wm) x (nb/wn) */
     int mfma_m, mfma_n, mfma_k;    /* instruction tile */
-    int vec;                       /* 1: 16-byte vector loads (aligned operands only) */
+    int vec;                       /* 1: needs 16-byte-aligned operand rows; 0: any element alignment */
     int family;                    /* 0: loads staged through registers, 1: direct-to-LDS DMA */
     int stages;                    /* LDS ring depth (K steps in flight + 1) */
     int threads;
@@ -100,7 +100,8 @@ typedef struct vx_plan {
     int kernel_id;
     int split_k;                   /* K slices reduced in fp32 by the last-arriving workgroup */
     int k_per_split;               /* K extent of one slice (a multiple of kb) */
-    int c_vec;                     /* 1: 4-element vector stores of C */
+    int c_vec;                     /* 1: C's rows are 4-element aligned (informational: full
+                                      4-column chunks of C are stored as one vector either way) */
     int64_t tiles_m, tiles_n;
     int64_t grid;                  /* workgroups launched */
     int group_m;
@@ -192,6 +193,19 @@ vx_status vx_kernel_occupancy(int kernel_id, int* wgs_per_cu);
  * VX_ERR_NO_CANDIDATE.
  */
 vx_status vx_force_plan(int kernel_id, int split_k);
+
+/*
+ * Hierarchy ablation (the Static1 variant of Section 7.4): restrict every
+ * following selection to kernels whose wavefront-level strategy is a
+ * wave_m x wave_n wavefront tile built from mfma_m x mfma_m MFMA instructions;
+ * the workgroup tile and the split stay dynamic.  (Static2, which also fixes
+ * the workgroup tile, is vx_force_plan(kernel_id, 0).)  All three 0 lifts the
+ * restriction.  VX_ERR_INVALID_ARG for a partly zero or negative triple,
+ * VX_ERR_NO_CANDIDATE if no enabled kernel has that strategy; calls whose
+ * dtype or alignment no such kernel serves return VX_ERR_NO_CANDIDATE.
+ * Process-wide; for studies and tests.
+ */
+vx_status vx_fix_wavefront(int wave_m, int wave_n, int mfma_m);
 
 /*
  * Hand the library a caller-owned device buffer to use as the split-K

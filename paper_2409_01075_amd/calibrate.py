@@ -91,10 +91,14 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
         def timed(M, N, K, split):
             set_bytes = (M * K + K * N + M * N) * eb
             R = int(min(max(2, -(-rot_mib * 2 ** 20 // set_bytes)), 512))
-            A = torch.randn((R, M * K), device=dev).to(tdt[k.dtype])
-            B = torch.randn((R, K * N), device=dev).to(tdt[k.dtype])
-            C = torch.empty((R, M * N), dtype=tdt[k.dtype], device=dev)
-            a0, b0, cc = A.data_ptr(), B.data_ptr(), C.data_ptr()
+            # element-aligned kernels are timed on operands shifted by one
+            # element, so that every row access is the misaligned kind they
+            # exist for
+            sh = 0 if k.vec else 1
+            A = torch.randn((R * M * K + sh,), device=dev).to(tdt[k.dtype])
+            B = torch.randn((R * K * N + sh,), device=dev).to(tdt[k.dtype])
+            C = torch.empty((R * M * N + sh,), dtype=tdt[k.dtype], device=dev)
+            a0, b0, cc = (X.data_ptr() + sh * eb for X in (A, B, C))
             sa, sb, sc = M * K * eb, K * N * eb, M * N * eb
             vx.vx_force_plan(kid, split)
             try:

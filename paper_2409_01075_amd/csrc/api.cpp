@@ -34,6 +34,7 @@ bool g_hw_valid[kMaxDevices];
 vx_hwinfo g_hw[kMaxDevices];
 std::atomic<int> g_force_id{-1};
 std::atomic<int> g_force_split{0};
+std::atomic<int> g_fix_wm{0}, g_fix_wn{0}, g_fix_mi{0};
 std::atomic<uint64_t> g_epoch{0};   // bumps when planning inputs change
 
 struct PlanKey {
@@ -202,7 +203,16 @@ vx_status current_device(int* dev)
 
 vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
 {
-    const int fid = g_force_id.load(), fsplit = g_force_split.load();
+    // the epoch is read before the filter: a setter changes the filter and
+    // then bumps the epoch, so a plan made under a stale filter is filed
+    // under a stale epoch and never found again
+    const uint64_t epoch = g_epoch.load();
+    VxFilter f;
+    f.kernel_id = g_force_id.load();
+    f.split = g_force_split.load();
+    f.wave_m = g_fix_wm.load();
+    f.wave_n = g_fix_wn.load();
+    f.mfma_m = g_fix_mi.load();
     vx_hwinfo hw;
     vx_status st = hwinfo_for(dev, &hw);
     if (st != VX_OK)
@@ -211,9 +221,9 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
     VxLimits lim;
     lim.ws_bytes = ws_bytes;
     lim.max_tickets = ws_bytes ? (int64_t)(kTicketBytes / 4) : 0;
-    if (fid >= 0)
-        return vxi_select(hw, sh, lim, fid, fsplit, out);
-    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, g_epoch.load()};
+    if (f.kernel_id >= 0)
+        return vxi_select(hw, sh, lim, f, out);
+    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, epoch};
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_plans.find(key);
@@ -222,7 +232,7 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
             return VX_OK;
         }
     }
-    st = vxi_select(hw, sh, lim, -1, 0, out);
+    st = vxi_select(hw, sh, lim, f, out);
     if (st != VX_OK)
         return st;
     std::lock_guard<std::mutex> lk(g_mu);
@@ -346,7 +356,6 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
     a.batch = (int)batch;
     a.group_m = plan.group_m;
     a.num_xcd = hw.num_xcd;
-    a.c_vec = plan.c_vec;
     a.ws = plan.split_k > 1 ? (float*)(ws.base + kTicketBytes) : nullptr;
     a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
     hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);
@@ -553,6 +562,39 @@ vx_status vx_force_plan(int kernel_id, int split_k)
         return VX_ERR_NO_CANDIDATE;
     g_force_id.store(kernel_id < 0 ? -1 : kernel_id);
     g_force_split.store(split_k > 0 ? split_k : 0);
+    return VX_OK;
+}
+
+vx_status vx_fix_wavefront(int wave_m, int wave_n, int mfma_m)
+{
+    if (wave_m == 0 && wave_n == 0 && mfma_m == 0) {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_fix_wm.store(0);
+        g_fix_wn.store(0);
+        g_fix_mi.store(0);
+        g_plans.clear();
+        g_epoch.fetch_add(1);
+        return VX_OK;
+    }
+    if (wave_m <= 0 || wave_n <= 0 || mfma_m <= 0)
+        return VX_ERR_INVALID_ARG;
+    VxFilter f;
+    f.wave_m = wave_m;
+    f.wave_n = wave_n;
+    f.mfma_m = mfma_m;
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    bool any = false;
+    for (int i = 0; i < n && !any; ++i)
+        any = reg[i].info.enabled && vxi_wave_matches(f, reg[i].info);
+    if (!any)
+        return VX_ERR_NO_CANDIDATE;
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_fix_wm.store(wave_m);
+    g_fix_wn.store(wave_n);
+    g_fix_mi.store(mfma_m);
+    g_plans.clear();
+    g_epoch.fetch_add(1);
     return VX_OK;
 }
 

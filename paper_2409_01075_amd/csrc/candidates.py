@@ -229,12 +229,14 @@ def _entry(dtype, family, stages, c, vec, hw):
 def registry(hw=GFX950):
     """All workgroup-level candidates that are compiled into the library.
 
-    fp16/bf16: direct-to-LDS tiles with 16-byte loads (aligned operands), each
-    with a 2-stage and with its deepest ring; register-staged tiles with
-    element-wise loads (any alignment; a 2-byte buffer-to-LDS load fills a
-    whole dword of LDS, so unaligned rows cannot be DMA'd densely); and a few
-    register-staged vector tiles for very large operands.
-    fp32: register-staged tiles, vector and element-wise."""
+    fp16/bf16: direct-to-LDS tiles with 16-byte loads (16-byte-aligned
+    operands), each with a 2-stage and with its deepest ring; register-staged
+    tiles for element-aligned operands (misaligned 16-byte row chunks; a
+    2-byte buffer-to-LDS load fills a whole dword of LDS, so unaligned rows
+    cannot be DMA'd densely); and a few register-staged 16-byte-aligned tiles
+    for very large operands.
+    fp32: register-staged tiles, each for 16-byte-aligned and for
+    element-aligned operands."""
     out = []
     for dtype in ("f16", "bf16"):
         for c in generate_candidates_for_layer(2, dtype, hw, "dma")[0]:

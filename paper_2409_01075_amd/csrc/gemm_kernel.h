@@ -33,12 +33,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+// The same vectors at element alignment.  The HSA runtime runs gfx9 memory in
+// unaligned mode, so these still compile to single 8/16-byte global accesses.
+typedef unsigned u32x4_u __attribute__((ext_vector_type(4), aligned(2)));
+typedef unsigned u32x2_u __attribute__((ext_vector_type(2), aligned(2)));
 
 enum { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
 
 // Compile-time description of one candidate: workgroup tile Mb x Nb x Kb,
-// WM x WN wavefronts, MFMA instruction tile MI x MI, vector (16-byte) or
-// element-wise global loads.
+// WM x WN wavefronts, MFMA instruction tile MI x MI, operands whose rows are
+// 16-byte aligned (VEC) or only element aligned.
 template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, bool VEC_>
 struct Cfg {
     static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_;
@@ -64,7 +68,7 @@ struct Cfg {
                                      : ((KB / 4) * (NB / 8) % NT == 0 && (KB / 4) * (NB / 8) >= NT) ? 4 : 2;
     static constexpr int KBB = KB / BK;                  // k-blocks per tile
     static constexpr int BBLK = H ? KBB * (NB / 8) / NT : 0;
-    // B tile, fp32: KB*NB/4 vectors along n; 16-bit element-wise path: NB*KB/8 k-vectors
+    // B tile, fp32: KB*NB/4 vectors along n
     static constexpr int BV = H ? NB * KB / 8 / NT : KB * NB / 4 / NT;
     static constexpr int KI = H ? (MI == 16 ? 32 : 16) : (MI == 16 ? 4 : 2);   // K per MFMA
     static constexpr int KCH = H ? KI : (MI == 16 ? 16 : 8);                      // K per fragment load
@@ -74,7 +78,7 @@ struct Cfg {
     static_assert(KB % KCH == 0, "Kb must be a multiple of the MFMA K chunk");
     static_assert(AV >= 1 && AV * VE * NT == MB * KB, "A tile must split evenly over threads");
     static_assert(BV >= 1 && (H ? BV * 8 : BV * 4) * NT == NB * KB, "B tile must split evenly over threads");
-    static_assert(!H || !VEC || (BBLK >= 1 && BBLK * NT * BK * 8 == KB * NB), "B blocks must split evenly");
+    static_assert(!H || (BBLK >= 1 && BBLK * NT * BK * 8 == KB * NB), "B blocks must split evenly");
     static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
 };
 
@@ -94,13 +98,18 @@ struct Tile {
     // Registers holding one K step of A and B between the global load and the
     // LDS store.
     u32x4 ra[C::AV];
-    u32x4 rb[C::H && C::VEC ? C::BBLK * C::BK : C::BV];
+    u32x4 rb[C::H ? C::BBLK * C::BK : C::BV];
 
-    // Global -> registers for the K step starting at k0 (< kend).
+    // Global -> registers for the K step starting at k0 (< kend).  Every
+    // thread moves 16-byte chunks of a row (8 elements of 16-bit data, 4 of
+    // fp32).  With VEC the rows are 16-byte aligned and a chunk is wholly in
+    // or out of range.  Otherwise a chunk wholly in range is still one
+    // (misaligned) 16-byte load, and only the chunk straddling the K or N edge
+    // is gathered element by element.
     __device__ __forceinline__ void load(const char* __restrict__ Ab, const char* __restrict__ Bb,
                                          int m0, int n0, int k0, int kend, int M, int N, int K, int t)
     {
-        // A: MB x KB, 16-byte vectors along k
+        // A: MB x KB, chunks along k
 #pragma unroll
         for (int v = 0; v < C::AV; ++v) {
             const int idx = t + v * C::NT;
@@ -112,23 +121,15 @@ struct Tile {
             } else {
                 u32x4 x = {0, 0, 0, 0};
                 if (gm < M) {
-                    if (C::H) {
-#pragma unroll
-                        for (int e = 0; e < 8; e += 2) {
-                            unsigned lo = gk + e < kend ? ((const uint16_t*)p)[e] : 0u;
-                            unsigned hi = gk + e + 1 < kend ? ((const uint16_t*)p)[e + 1] : 0u;
-                            x[e >> 1] = pack2(lo, hi);
-                        }
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            x[e] = gk + e < kend ? ((const unsigned*)p)[e] : 0u;
-                    }
+                    if (gk + C::VE <= kend)
+                        x = *(const u32x4_u*)p;
+                    else
+                        x = gather_row(p, kend - gk);
                 }
                 ra[v] = x;
             }
         }
-        if (C::H && C::VEC) {
+        if (C::H) {
             // B: blocks of BK rows x 8 columns (16 bytes per row)
 #pragma unroll
             for (int i = 0; i < C::BBLK; ++i) {
@@ -139,30 +140,22 @@ struct Tile {
                 for (int r = 0; r < C::BK; ++r) {
                     const int gk = k0 + kb * C::BK + r;
                     const char* p = Bb + ((int64_t)gk * N + gn) * 2;
-                    rb[i * C::BK + r] = (gk < kend && gn < N) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
-                }
-            }
-        } else if (C::H) {
-            // B, element-wise: each thread gathers 8 consecutive k of one column
-#pragma unroll
-            for (int v = 0; v < C::BV; ++v) {
-                const int idx = t + v * C::NT;
-                const int n = idx % C::NB, kv = idx / C::NB;
-                const int gn = n0 + n, gk = k0 + kv * 8;
-                const uint16_t* p = (const uint16_t*)Bb + (int64_t)gk * N + gn;
-                u32x4 x = {0, 0, 0, 0};
-                if (gn < N) {
-#pragma unroll
-                    for (int e = 0; e < 8; e += 2) {
-                        unsigned lo = gk + e < kend ? p[(int64_t)e * N] : 0u;
-                        unsigned hi = gk + e + 1 < kend ? p[(int64_t)(e + 1) * N] : 0u;
-                        x[e >> 1] = pack2(lo, hi);
+                    if (C::VEC) {
+                        rb[i * C::BK + r] = (gk < kend && gn < N) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
+                    } else {
+                        u32x4 x = {0, 0, 0, 0};
+                        if (gk < kend) {
+                            if (gn + 8 <= N)
+                                x = *(const u32x4_u*)p;
+                            else
+                                x = gather_row(p, N - gn);
+                        }
+                        rb[i * C::BK + r] = x;
                     }
                 }
-                rb[v] = x;
             }
         } else {
-            // fp32 B: natural layout, 4 consecutive columns per vector
+            // fp32 B: natural layout, 4 consecutive columns per chunk
 #pragma unroll
             for (int v = 0; v < C::BV; ++v) {
                 const int idx = t + v * C::NT;
@@ -174,14 +167,34 @@ struct Tile {
                 } else {
                     u32x4 x = {0, 0, 0, 0};
                     if (gk < kend) {
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            x[e] = gn + e < N ? ((const unsigned*)p)[e] : 0u;
+                        if (gn + 4 <= N)
+                            x = *(const u32x4_u*)p;
+                        else
+                            x = gather_row(p, N - gn);
                     }
                     rb[v] = x;
                 }
             }
         }
+    }
+
+    // The first `valid` (< one chunk) elements of a row chunk, zeros after.
+    __device__ __forceinline__ static u32x4 gather_row(const char* p, int valid)
+    {
+        u32x4 x = {0, 0, 0, 0};
+        if (C::H) {
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const unsigned lo = e < valid ? ((const uint16_t*)p)[e] : 0u;
+                const unsigned hi = e + 1 < valid ? ((const uint16_t*)p)[e + 1] : 0u;
+                x[e >> 1] = pack2(lo, hi);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                x[e] = e < valid ? ((const unsigned*)p)[e] : 0u;
+        }
+        return x;
     }
 
     // Registers -> LDS stage.
@@ -195,7 +208,7 @@ struct Tile {
             const int r = idx / (C::KB / C::VE), c = idx % (C::KB / C::VE);
             *(u32x4*)(As + (r * C::LDA + c * C::VE) * C::EB) = ra[v];
         }
-        if (C::H && C::VEC) {
+        if (C::H) {
             // transpose each BK x 8 block into 8 k-vectors (one per column)
 #pragma unroll
             for (int i = 0; i < C::BBLK; ++i) {
@@ -221,13 +234,6 @@ struct Tile {
                         *(unsigned*)dst = pack2(elem16(in[0], j), elem16(in[1], j));
                     }
                 }
-            }
-        } else if (C::H) {
-#pragma unroll
-            for (int v = 0; v < C::BV; ++v) {
-                const int idx = t + v * C::NT;
-                const int n = idx % C::NB, kv = idx / C::NB;
-                *(u32x4*)(Bs + (n * C::LDB + kv * 8) * 2) = rb[v];
             }
         } else {
 #pragma unroll
@@ -322,13 +328,15 @@ __device__ __forceinline__ void compute_step(const char* __restrict__ stage, Acc
 }
 
 // ---------------------------------------------------------------- Store ----
+// Four consecutive outputs of one C row: one 16/8-byte store when all four
+// are inside the row (at any element alignment), else element stores.
 template <int DT>
-__device__ __forceinline__ void store4(char* __restrict__ Cb, int64_t off, int n, int N, bool vec, float a0, float a1, float a2, float a3)
+__device__ __forceinline__ void store4(char* __restrict__ Cb, int64_t off, int n, int N, float a0, float a1, float a2, float a3)
 {
     if (DT == DT_F32) {
         float* p = (float*)Cb + off;
-        if (vec && n + 3 < N) {
-            *(f32x4*)p = f32x4{a0, a1, a2, a3};
+        if (n + 3 < N) {
+            *(u32x4_u*)p = __builtin_bit_cast(u32x4, f32x4{a0, a1, a2, a3});
         } else {
             if (n < N) p[0] = a0;
             if (n + 1 < N) p[1] = a1;
@@ -349,8 +357,8 @@ __device__ __forceinline__ void store4(char* __restrict__ Cb, int64_t off, int n
             h[3] = __builtin_bit_cast(uint16_t, (__bf16)a3);
         }
         uint16_t* p = (uint16_t*)Cb + off;
-        if (vec && n + 3 < N) {
-            *(u32x2*)p = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+        if (n + 3 < N) {
+            *(u32x2_u*)p = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
         } else {
             if (n < N) p[0] = h[0];
             if (n + 1 < N) p[1] = h[1];
@@ -497,7 +505,6 @@ __device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const G
 
     char* Cb = (char*)p.C + (int64_t)g.b * p.sC * C::EB;
     constexpr int NG = C::ACC / 4;
-    const bool cvec = p.c_vec != 0;
 #pragma unroll
     for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
@@ -509,7 +516,7 @@ __device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const G
                 const int m = g.m0 + wm0 + fm * C::MI + dm;
                 const int n = g.n0 + wn0 + fn * C::MI + dn;
                 if (m < p.M)
-                    store4<C::DT>(Cb, (int64_t)m * p.N + n, n, p.N, cvec,
+                    store4<C::DT>(Cb, (int64_t)m * p.N + n, n, p.N,
                                   acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1],
                                   acc.v[fn][fm][4 * gi + 2], acc.v[fn][fm][4 * gi + 3]);
             }

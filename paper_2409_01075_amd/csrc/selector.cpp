@@ -131,7 +131,10 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
 
     // Level 1: the K loop of one workgroup (Eq. 2 over n_k K steps).
     const double bw_wg = hw.l2_bytes_clk_cu * hw.clock_ghz / per_cu;                // B/ns
-    const double load_factor = k.vec ? 1.0 : 4.0;   // element-wise loads: 8x the instructions
+    // element-aligned operands: the same 16-byte loads, but misaligned ones
+    // straddle an extra cache line per row segment and the ragged edge chunks
+    // are gathered element by element
+    const double load_factor = k.vec ? 1.0 : 1.25;
     const double xfer = (double)(k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
     const double t_load = hw.mem_latency_ns + xfer;
     double t_store = (double)k.mb * k.nb * eb / bw_wg;
@@ -174,16 +177,24 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     return hw.launch_ns + std::max(cost2, floor_ns);
 }
 
-vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim, int forced_id,
-                     int forced_split, vx_plan* out)
+bool vxi_wave_matches(const VxFilter& f, const vx_kernel_info& k)
 {
+    if (f.wave_m <= 0)
+        return true;
+    return k.mb / k.wm == f.wave_m && k.nb / k.wn == f.wave_n && k.mfma_m == f.mfma_m;
+}
+
+vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim, const VxFilter& f,
+                     vx_plan* out)
+{
+    const int forced_id = f.kernel_id, forced_split = f.split;
     int n = 0;
     const VxKernelEntry* reg = vxi_registry(&n);
     double best = INFINITY;
     int best_id = -1, best_split = 0, best_kps = 0;
     for (int i = 0; i < n; ++i) {
         const vx_kernel_info& k = reg[i].info;
-        if (forced_id >= 0 && k.id != forced_id)
+        if ((forced_id >= 0 && k.id != forced_id) || !vxi_wave_matches(f, k))
             continue;
         for (int s : kSplits) {
             int split = s;

@@ -14,7 +14,6 @@ struct VxGemmArgs {
     int batch;
     int group_m;            // tile rows walked together by the grid-level order
     int num_xcd;            // workgroups are dispatched round-robin over this many XCDs
-    int c_vec;              // 1: C rows allow 4-element vector stores
     float* ws;              // split-K partial tiles (split > 1), fp32
     unsigned* tickets;      // one self-resetting arrival counter per output tile
 };

@@ -54,11 +54,20 @@ int vxi_occupancy(const vx_hwinfo& hw, const vx_kernel_info& k);
 double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k, int split,
                 const VxLimits& lim, int* k_per_split);
 
-// Argmin over the registry (Equation 1).  forced_id >= 0 restricts the search
-// to that kernel; forced_split > 0 to that split.  Returns VX_OK or
-// VX_ERR_NO_CANDIDATE.
-vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim, int forced_id,
-                     int forced_split, vx_plan* out);
+// Restrictions of the search, for tests and the hierarchy ablations.
+struct VxFilter {
+    int kernel_id = -1;   // >= 0: only this kernel (a fixed workgroup and wavefront strategy)
+    int split = 0;        // > 0: only this split-K factor
+    int wave_m = 0, wave_n = 0, mfma_m = 0;   // > 0: only kernels with this wavefront strategy
+};
+
+// True if kernel k passes the wavefront part of the filter.
+bool vxi_wave_matches(const VxFilter& f, const vx_kernel_info& k);
+
+// Argmin over the registry (Equation 1) among the kernels and splits the
+// filter admits.  Returns VX_OK or VX_ERR_NO_CANDIDATE.
+vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim, const VxFilter& f,
+                     vx_plan* out);
 
 // grid-level tile order: tile rows walked together (bounded by the tile count)
 int vxi_group_m(int64_t tiles_m, int64_t tiles_n);

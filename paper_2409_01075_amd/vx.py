@@ -57,6 +57,12 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError("libvx.so not built: run `python -m paper_2409_01075_amd.build` "
                            "(or __graft_entry__.build())")
+    # PyTorch bundles its own HIP runtime (soname libamdhip64.so.7, but its
+    # libraries ask for it as libamdhip64.so).  Loaded first, it also
+    # satisfies this library's libamdhip64.so.7; loaded after this library,
+    # it would come in as a second HIP runtime beside the system one, and the
+    # two would not share devices, streams or allocations.  So torch goes first.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
     L.vx_gemm.argtypes = [i64, i64, i64, i32, vp, vp, vp, vp]
@@ -81,6 +87,8 @@ def lib():
     L.vx_registry_get.restype = i32
     L.vx_force_plan.argtypes = [i32, i32]
     L.vx_force_plan.restype = i32
+    L.vx_fix_wavefront.argtypes = [i32, i32, i32]
+    L.vx_fix_wavefront.restype = i32
     L.vx_set_workspace.argtypes = [vp, ctypes.c_size_t, vp]
     L.vx_set_workspace.restype = i32
     L.vx_calibration_load.argtypes = [ctypes.c_char_p, ctypes.POINTER(i32)]
@@ -159,6 +167,10 @@ def vx_registry_get(i):
 
 def vx_force_plan(kernel_id, split_k=0):
     return lib().vx_force_plan(kernel_id, split_k)
+
+
+def vx_fix_wavefront(wave_m=0, wave_n=0, mfma_m=0):
+    return lib().vx_fix_wavefront(wave_m, wave_n, mfma_m)
 
 
 def vx_set_workspace(ptr, nbytes, stream=None):

@@ -260,3 +260,52 @@ def test_force_plan_validation():
     assert vx.vx_force_plan(vx.vx_registry_count(), 1) == 3
     assert vx.vx_force_plan(0, 2) == 0
     assert vx.vx_force_plan(-1, 0) == 0
+
+
+def test_fix_wavefront_restricts_the_argmin(mi355x_override):
+    """The Static1 ablation: with a fixed wavefront strategy the selector
+    returns the cheapest plan among exactly the kernels that have it, and
+    lifting the restriction restores the unrestricted plan."""
+    assert vx.vx_fix_wavefront(32, 0, 16) == 1
+    assert vx.vx_fix_wavefront(-32, 32, 16) == 1
+    assert vx.vx_fix_wavefront(24, 24, 16) == 3
+    reg = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]
+
+    def wave(k):
+        return (k.mb // k.wm, k.nb // k.wn, k.mfma_m)
+
+    splits = (1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32)
+    strat = (32, 32, 16)
+    try:
+        for (b, M, N, K, dt) in [(1, 77, 768, 768, 1), (1, 3000, 4096, 4096, 2), (4, 100, 200, 300, 0)]:
+            p0 = vx.vx_plan_query(b, M, N, K, dt)
+            assert vx.vx_fix_wavefront(*strat) == 0
+            p = vx.vx_plan_query(b, M, N, K, dt)
+            assert wave(p.kernel) == strat
+            assert p.predicted_ns >= p0.predicted_ns
+            best = min(c for k in reg if k.enabled and k.dtype == dt and wave(k) == strat for s in splits
+                       for st, c in [vx.vx_plan_cost(b, M, N, K, dt, k.id, s, 1)] if st == 0)
+            assert p.predicted_ns == pytest.approx(best, rel=1e-12)
+            assert vx.vx_fix_wavefront(0, 0, 0) == 0
+            p1 = vx.vx_plan_query(b, M, N, K, dt)
+            assert (p1.kernel_id, p1.split_k) == (p0.kernel_id, p0.split_k)
+        # a strategy that only disabled (spilling) kernels have is refused
+        disabled_only = {wave(k) for k in reg if not k.enabled} - {wave(k) for k in reg if k.enabled}
+        assert disabled_only
+        assert vx.vx_fix_wavefront(*sorted(disabled_only)[0]) == 3
+    finally:
+        assert vx.vx_fix_wavefront(0, 0, 0) == 0
+
+
+def test_one_hip_runtime_when_the_binding_loads_first():
+    """Loading the library before anything else imports torch must not bring
+    a second HIP runtime into the process (torch bundles its own)."""
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2409_01075_amd import vx\n"
+            "vx.lib()\n"
+            "import torch\n"
+            "maps = open('/proc/self/maps').read()\n"
+            "print(len({l.split()[-1] for l in maps.splitlines() if 'libamdhip64' in l}))\n" % ROOT)
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.strip().splitlines()[-1] == "1"

@@ -75,7 +75,7 @@ def test_llm_trial(trial):
 
 def test_attention_unaligned_lengths():
     """L values that break every vector alignment (odd, prime) use the
-    element-wise kernels; checked in full at a reduced batch."""
+    element-aligned register-staged kernels; checked in full at a reduced batch."""
     g = I.rng(3100)
     for L in (1, 7, 37, 129, 255):
         b, d = 6, 64
