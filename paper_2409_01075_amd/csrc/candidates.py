@@ -19,7 +19,8 @@ workgroup level):
   * "dma": fp16/bf16 tiles loaded by 16-byte buffer-load-to-LDS instructions
     into a ring of STAGES LDS stages (no VGPR staging); B keeps its
     n-contiguous layout and is read with the transposing LDS read.  Each tile
-    is offered with 2 stages and with the deepest ring (3 or 4) that fits.
+    is offered with 2 stages, with the deepest ring of 3 or 4, and with the
+    deepest of 5..16 that fits (a whole short K range in flight).
   * "reg": loads staged through VGPRs into a 2-stage LDS ring (fp32; fp16/bf16
     operands that are not 16-byte aligned; a few fp16/bf16 tiles for operands
     whose byte extents exceed 32-bit buffer offsets).
@@ -30,8 +31,8 @@ this library's reading):
   * L1: accumulator registers Mw*Nw/64 in [4, 128] of the 512 per lane for
     register-staged tiles (staging, fragments and addresses must fit beside
     them), [4, 256] for direct-to-LDS tiles (no staging registers); aspect <= 4.
-  * L2: 4 wavefronts per workgroup (one per SIMD of the CU), or 8 for tiles of
-    at least 128 x 128; LDS for a 2-stage ring <= 160 KiB; the K step reads at
+  * L2: 4 wavefronts per workgroup (one per SIMD of the CU), 8 for tiles of
+    at least 128 x 128, 1 or 2 for tiles of at most 512 outputs (16 x 16, 16 x 32, 32 x 16); LDS for a 2-stage ring <= 160 KiB; the K step reads at
     least 128 contiguous bytes per row (two 64-byte segments); aspect of the
     workgroup tile <= 8.  DMA tiles: A and B split into whole 1 KiB wave
     transfers per K step.  Register-staged tiles: every thread moves at least
@@ -118,9 +119,15 @@ def lds_bytes_dma(mb, nb, kb, stages):
     return stages * (mb * kb + kb * nb) * 2
 
 
+DEEP_MAX = 16   # deepest ring offered (K steps in flight = stages - 1)
+
+
 def dma_stage_options(mb, nb, kb, wm, wn, mi, vec, hw):
-    """Pipeline depths offered for a DMA tile: 2 and the deepest of 3..4 that
-    fits the LDS and the 6-bit vmcnt of the waits."""
+    """Pipeline depths offered for a DMA tile: 2, the deepest of 3..4, and
+    the deepest of 5..DEEP_MAX, each if it fits the LDS and the 6-bit vmcnt
+    of the waits.  Deep rings keep a whole short K range in flight at once:
+    a latency-bound call then waits for one memory round trip instead of
+    one per group of STAGES-1 K steps."""
     nwave = wm * wn
     lane = 16 if vec else 2
     wave_bytes = 64 * lane
@@ -128,11 +135,13 @@ def dma_stage_options(mb, nb, kb, wm, wn, mi, vec, hw):
     if a_bytes % (wave_bytes * nwave) or b_bytes % (wave_bytes * nwave):
         return []
     lps = a_bytes // (wave_bytes * nwave) + b_bytes // (wave_bytes * nwave)
-    ok = [st for st in (2, 3, 4)
-          if lds_bytes_dma(mb, nb, kb, st) <= hw["lds_bytes"] - LDS_RESERVE and (st - 2) * lps <= 63]
+    def fits(st):
+        return lds_bytes_dma(mb, nb, kb, st) <= hw["lds_bytes"] - LDS_RESERVE and (st - 1) * lps <= 63
+    ok = [st for st in (2, 3, 4) if fits(st)]
     if not ok:
         return []
-    return sorted({ok[0], ok[-1]})
+    deep = [st for st in range(5, DEEP_MAX + 1) if fits(st)]
+    return sorted({ok[0], ok[-1]} | set(deep[-1:]))
 
 
 def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw, family):
@@ -142,7 +151,10 @@ def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw, family):
     if nt > hw["max_threads"]:
         return False
     waves = wm * wn
-    if waves != 4 and not (waves == 8 and mb >= 128 and nb >= 128):
+    # one wavefront per SIMD; 8 for large tiles; 1 or 2 for small tiles, which
+    # give latency-bound calls (small M, or small N) more workgroups to spread
+    # over the CUs
+    if not (waves == 4 or (waves == 8 and mb >= 128 and nb >= 128) or (waves <= 2 and mb * nb <= 512)):
         return False
     if max(mb, nb) > 8 * min(mb, nb) or max(mb, nb) > 256:
         return False

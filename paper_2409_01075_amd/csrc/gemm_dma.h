@@ -44,7 +44,7 @@ struct DCfg {
     static constexpr int KI = MI == 16 ? 32 : 16;
     static constexpr int A_BYTES = MB * KB * 2, B_BYTES = KB * NB * 2;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-    static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;   // one object per stage
+    static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;   // the whole ring
     static constexpr int CPA = KB / 8, CPB = NB / 8;       // 16-byte chunks per row
     static constexpr int SWA = CPA < 16 ? CPA : 16;        // A swizzle period (rows)
     static constexpr int LANE_BYTES = 16;                  // bytes one lane moves per DMA instruction
@@ -58,8 +58,8 @@ struct DCfg {
     static_assert(KB % KI == 0 && KB % 8 == 0 && NB % 8 == 0, "K step and chunking");
     static_assert(A_IPW >= 1 && A_IPW * WAVE_BYTES * NWAVE == A_BYTES, "A DMA must split evenly over waves");
     static_assert(B_IPW >= 1 && B_IPW * WAVE_BYTES * NWAVE == B_BYTES, "B DMA must split evenly over waves");
-    static_assert(STAGES >= 2 && STAGES <= 4, "pipeline depth");
-    static_assert((STAGES - 2) * LPS <= 63, "vmcnt range");
+    static_assert(STAGES >= 2 && STAGES <= 16, "pipeline depth");
+    static_assert((STAGES - 1) * LPS <= 63, "vmcnt range: the prologue's DMA all in flight");
     static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
 };
 
@@ -73,6 +73,21 @@ __device__ __forceinline__ void wait_vm()
 {
     static_assert(N >= 0 && N <= 63, "vmcnt range");
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Waits until at most min(r, R) K steps of LPS DMA instructions each are in
+// flight (r >= 0 is wave-uniform; s_waitcnt takes only immediates).
+template <int LPS, int R>
+__device__ __forceinline__ void wait_steps(int r)
+{
+    if constexpr (R <= 0) {
+        wait_vm<0>();
+    } else {
+        if (r >= R)
+            wait_vm<R * LPS>();
+        else
+            wait_steps<LPS, R - 1>(r);
+    }
 }
 
 constexpr unsigned kOOB = 0x80000000u;    // buffer offset beyond every resource's range
@@ -185,15 +200,11 @@ __device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm
 template <class C>
 __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& p)
 {
-    // One LDS object per stage: distinct objects let the compiler see that a
-    // DMA into one stage never aliases the reads of another, so it leaves the
-    // loads in flight and the pipeline waits only where wait_steps says.
+    // The ring: STAGES stages of one K step each.  Stage indices are
+    // compile-time constants in the unrolled main loop below.
     constexpr int SB = C::STAGE_BYTES;
-    __shared__ __attribute__((aligned(1024))) char st0[SB];
-    __shared__ __attribute__((aligned(1024))) char st1[SB];
-    __shared__ __attribute__((aligned(1024))) char st2[C::STAGES > 2 ? SB : 16];
-    __shared__ __attribute__((aligned(1024))) char st3[C::STAGES > 3 ? SB : 16];
-#define VX_STAGE(j) ((lds_char*)((j) == 0 ? st0 : (j) == 1 ? st1 : (j) == 2 ? st2 : st3))
+    __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
+#define VX_STAGE(j) ((lds_char*)smem + (j) * SB)
 
     const int t = threadIdx.x;
     const int lane = t & 63;
@@ -208,14 +219,15 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& p)
     Acc<C> acc;
     acc_zero<C>(acc);
 
-    // Every DMA is issued unconditionally: a step beyond the slice gets only
-    // out-of-range offsets (zero fill, no memory traffic).  Without branches
-    // around the DMAs the number in flight is the same at every wait, and the
-    // compiler's own wait tracking stays exact across the loop.
-    // prologue: the first STAGES-1 K steps, step s into stage s
+    // Only the slice's own K steps are issued: a DMA instruction costs issue
+    // time even when all its offsets are out of range.  While the ring is
+    // full, STAGES-2 steps stay in flight behind the one waited for; in the
+    // last STAGES-2 iterations (the drain) the count falls to 0.
+    // prologue: the first min(STAGES-1, nk) K steps, step s into stage s
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s)
-        DmaTile<C>::issue(VX_STAGE(s), Apanel, Bbatch, g.kbeg + s * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
+        if (s < g.nk)
+            DmaTile<C>::issue(VX_STAGE(s), Apanel, Bbatch, g.kbeg + s * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
     // main loop, unrolled by STAGES so that every stage index is a constant
     for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
 #pragma unroll
@@ -223,14 +235,15 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& p)
             const int it = it0 + j;
             if (it >= g.nk)
                 break;
-            wait_vm<(C::STAGES - 2) * C::LPS>();   // step `it` has landed (this wave's part)
-            __builtin_amdgcn_s_barrier();          // ... and every wave's; stage it-1 is free
-            DmaTile<C>::issue(VX_STAGE((j + C::STAGES - 1) % C::STAGES), Apanel, Bbatch,
-                              g.kbeg + (it + C::STAGES - 1) * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
+            wait_steps<C::LPS, C::STAGES - 2>(g.nk - 1 - it);   // step `it` has landed (this wave's part)
+            __builtin_amdgcn_s_barrier();                      // ... and every wave's; stage it-1 is free
+            if (it + C::STAGES - 1 < g.nk)
+                DmaTile<C>::issue(VX_STAGE((j + C::STAGES - 1) % C::STAGES), Apanel, Bbatch,
+                                  g.kbeg + (it + C::STAGES - 1) * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
             dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane);
         }
     }
-    wait_vm<0>();   // drain the zero-fill DMAs before LDS is released
+    wait_vm<0>();   // nothing is in flight here; kept as a guard before LDS is released
 #undef VX_STAGE
     finish<C>(p, acc, g, t, lane, wm0, wn0);
 }

@@ -477,6 +477,32 @@ __device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const G
         if (arrived != (unsigned)(p.split - 1))
             return;
         static_assert(PER % 4 == 0, "accumulators come in groups of 4");
+        // Sum slices 0..split-1 in order.  The loads of SF slices are issued
+        // together before any of them is added, so the reduction waits for one
+        // memory round trip per SF slices rather than one per slice (the last
+        // slice's own partial is read back like the others: it is complete).
+        constexpr int SF = P4 <= 2 ? 8 : P4 <= 4 ? 4 : P4 <= 8 ? 2 : 1;
+        f32x4 sum[P4];
+        for (int zz0 = 0; zz0 < p.split; zz0 += SF) {
+            f32x4 part[SF][P4];
+#pragma unroll
+            for (int j = 0; j < SF; ++j) {
+                const int zz = min(zz0 + j, p.split - 1);   // in range; surplus loads are not added
+#pragma unroll
+                for (int e4 = 0; e4 < P4; ++e4)
+                    part[j][e4] = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, zz * SLICE_BYTES + (unsigned)(e4 * C::NT + t) * 16,
+                                                                     0, SC1));
+            }
+#pragma unroll
+            for (int j = 0; j < SF; ++j) {
+                if (zz0 + j >= p.split)
+                    break;
+#pragma unroll
+                for (int e4 = 0; e4 < P4; ++e4)
+                    sum[e4] = zz0 + j == 0 ? part[j][e4] : sum[e4] + part[j][e4];
+            }
+        }
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
@@ -484,20 +510,9 @@ __device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const G
 #pragma unroll
                 for (int gi = 0; gi < C::ACC / 4; ++gi) {
                     const int e4 = (fn * C::FM + fm) * (C::ACC / 4) + gi;
-                    const unsigned off = (unsigned)(e4 * C::NT + t) * 16;
-                    f32x4 own = {acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1], acc.v[fn][fm][4 * gi + 2],
-                                 acc.v[fn][fm][4 * gi + 3]};
-                    f32x4 sum = g.z == 0 ? own
-                                         : __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, SC1));
-                    for (int zz = 1; zz < p.split; ++zz) {
-                        const f32x4 part = zz == g.z ? own
-                                                     : __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                                                     rw, zz * SLICE_BYTES + off, 0, SC1));
-                        sum += part;
-                    }
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        acc.v[fn][fm][4 * gi + e] = sum[e];
+                        acc.v[fn][fm][4 * gi + e] = sum[e4][e];
                 }
         if (t == 0)
             __hip_atomic_store(&p.tickets[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -171,6 +171,30 @@ def test_every_kernel_integer_exact(code):
     assert ran > 0
 
 
+@pytest.mark.parametrize("code", [1, 2])
+def test_every_ring_kernel_long_k(code):
+    """Each direct-to-LDS kernel on a K range longer than its LDS ring: the
+    prologue, the steady state with the ring full, the wrap of the stage
+    index and the drain all run (plus a K tail in the last step)."""
+    g = I.rng(450 + code)
+    ran = 0
+    for k in _kernel_cases():
+        if k.dtype != code or not k.enabled or k.family != 1:
+            continue
+        M, N, _ = _shape_for(k)
+        K = (k.stages + 2) * k.kb + 8
+        r = max(1, min(4, I.exact_range(K, code)))
+        A = I.small_int(g, (M, K), code, -r, r)
+        B = I.small_int(g, (K, N), code, -r, r)
+        assert vx.vx_force_plan(k.id, 1) == 0
+        C = run_gemm(A, B, code)
+        vx.vx_force_plan(-1, 0)
+        tolerance.check_exact(C, oracle.gemm(A, B, code, with_mag=False), code,
+                              "kernel %d %s stages %d K %d" % (k.id, (k.mb, k.nb, k.kb, k.wm, k.wn), k.stages, K))
+        ran += 1
+    assert ran > 0
+
+
 @pytest.mark.parametrize("code", DTS)
 @pytest.mark.parametrize("split", [2, 3, 5, 8])
 def test_split_k_integer_exact(code, split):
