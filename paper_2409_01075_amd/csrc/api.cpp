@@ -356,6 +356,7 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
     a.batch = (int)batch;
     a.group_m = plan.group_m;
     a.num_xcd = hw.num_xcd;
+    a.grid = (int)plan.grid;
     a.ws = plan.split_k > 1 ? (float*)(ws.base + kTicketBytes) : nullptr;
     a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
     hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);

@@ -198,8 +198,9 @@ __device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm
 }
 
 template <class C>
-__device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& p)
+__device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
 {
+    const VxGemmArgs p = pin_args(args);
     // The ring: STAGES stages of one K step each.  Stage indices are
     // compile-time constants in the unrolled main loop below.
     constexpr int SB = C::STAGE_BYTES;

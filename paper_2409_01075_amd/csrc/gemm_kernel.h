@@ -382,6 +382,21 @@ __device__ __forceinline__ void acc_coord(int lane, int g, int& dm, int& dn)
     }
 }
 
+// Kernel arguments, all in SGPRs from the first instructions on.  Left to
+// itself the compiler sinks each kernarg load next to its first use and
+// waits for each batch in turn; the argument block is not cached at kernel
+// start, so every batch costs a memory round trip before the first operand
+// load can be issued.  Pinning every field at entry issues all the loads
+// together and waits once.
+__device__ __forceinline__ VxGemmArgs pin_args(const VxGemmArgs& in)
+{
+    VxGemmArgs p = in;
+    asm volatile("" : "+s"(p.A), "+s"(p.B), "+s"(p.C), "+s"(p.sA), "+s"(p.sB), "+s"(p.sC), "+s"(p.M), "+s"(p.N),
+                      "+s"(p.K), "+s"(p.tiles_m), "+s"(p.tiles_n), "+s"(p.split), "+s"(p.k_per_split),
+                      "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.ws), "+s"(p.tickets));
+    return p;
+}
+
 // ---------------------------------------------------------- level 2 -------
 // Grid level: the parallel loop over (batch, K slice, tile) of one launch.
 struct GridPos {
@@ -394,7 +409,7 @@ __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
     // Workgroups are dispatched round-robin over the XCDs; remap the linear id
     // so that each XCD receives a contiguous range of logical tiles
     // (neighbouring tiles share A or B panels in that XCD's L2).
-    const int G = gridDim.x, w = blockIdx.x;
+    const int G = p.grid, w = blockIdx.x;
     const int nx = p.num_xcd;
     const int xcd = w % nx, q = G / nx, rem = G % nx;
     const int wl = xcd * q + (xcd < rem ? xcd : rem) + w / nx;
@@ -541,8 +556,9 @@ __device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const G
 // Level 1 with loads staged through VGPRs (any dtype; 16-bit B is transposed
 // in registers on its way into LDS).
 template <class C>
-__device__ __forceinline__ void gemm_body(const VxGemmArgs& p)
+__device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
 {
+    const VxGemmArgs p = pin_args(args);
     __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
 
     const int t = threadIdx.x;

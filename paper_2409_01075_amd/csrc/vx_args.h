@@ -14,6 +14,7 @@ struct VxGemmArgs {
     int batch;
     int group_m;            // tile rows walked together by the grid-level order
     int num_xcd;            // workgroups are dispatched round-robin over this many XCDs
+    int grid;               // workgroups in the launch: tiles_m * tiles_n * split * batch
     float* ws;              // split-K partial tiles (split > 1), fp32
     unsigned* tickets;      // one self-resetting arrival counter per output tile
 };
