@@ -23,13 +23,8 @@
 namespace vxk {
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
-// LDS addresses stay in address space 3 from the __shared__ object onwards:
-// the compiler's wait tracking for LDS DMA needs to see which object each
-// DMA and each read touches, and a detour through generic pointers hides it.
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_>
 struct DCfg {
@@ -53,10 +48,7 @@ struct DCfg {
     static constexpr int B_IPW = B_BYTES / WAVE_BYTES / NWAVE;
     static constexpr int LPS = A_IPW + B_IPW;
 
-    // Epilogue through LDS: the finished tile is written to the (then idle)
-    // ring as 16-bit values in rows padded by 16 bytes, and goes out as
-    // 16-byte chunks of whole rows, so a wave's store covers whole 128-byte
-    // lines instead of 8 bytes in each of 16 or 32 rows.
+    // epilogue through LDS (store_lds) when the C tile fits the idle ring
     static constexpr int LDC = NB + 8;
     static constexpr bool LDS_EPI = MB * LDC * 2 <= LDS_BYTES;
 
@@ -201,71 +193,6 @@ __device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm
                 else
                     mfma32<C::DT>(fb[fn], fa[fm], acc.v[fn][fm]);
             }
-    }
-}
-
-// Four fp32 values -> four 16-bit outputs (round to nearest even), packed.
-template <int DT>
-__device__ __forceinline__ u32x2 pack4_16(float a0, float a1, float a2, float a3)
-{
-    unsigned h0, h1, h2, h3;
-    if (DT == DT_F16) {
-        h0 = __builtin_bit_cast(uint16_t, (_Float16)a0);
-        h1 = __builtin_bit_cast(uint16_t, (_Float16)a1);
-        h2 = __builtin_bit_cast(uint16_t, (_Float16)a2);
-        h3 = __builtin_bit_cast(uint16_t, (_Float16)a3);
-    } else {
-        h0 = __builtin_bit_cast(uint16_t, (__bf16)a0);
-        h1 = __builtin_bit_cast(uint16_t, (__bf16)a1);
-        h2 = __builtin_bit_cast(uint16_t, (__bf16)a2);
-        h3 = __builtin_bit_cast(uint16_t, (__bf16)a3);
-    }
-    return u32x2{pack2(h0, h1), pack2(h2, h3)};
-}
-
-// The epilogue through LDS (see DCfg::LDS_EPI).  Every wave must be done with
-// the ring's last stage when this starts; the caller's barrier ensures it.
-template <class C>
-__device__ __forceinline__ void store_lds(const VxGemmArgs& p, Acc<C>& acc, const GridPos& g, int t, int lane, int wm0,
-                                          int wn0, lds_char* buf)
-{
-    // accumulators -> 16-bit -> LDS tile [MB][LDC]
-#pragma unroll
-    for (int fn = 0; fn < C::FN; ++fn)
-#pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm)
-#pragma unroll
-            for (int gi = 0; gi < C::ACC / 4; ++gi) {
-                int dm, dn;
-                acc_coord<C::MI>(lane, gi, dm, dn);
-                const int r = wm0 + fm * C::MI + dm, c = wn0 + fn * C::MI + dn;
-                *(__attribute__((address_space(3))) u32x2*)(buf + (r * C::LDC + c) * 2) =
-                    pack4_16<C::DT>(acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1], acc.v[fn][fm][4 * gi + 2],
-                                    acc.v[fn][fm][4 * gi + 3]);
-            }
-    __syncthreads();
-    // LDS -> C: consecutive threads take consecutive 16-byte chunks of a row
-    constexpr int CPR = C::NB / 8, CHUNKS = C::MB * CPR;
-    char* Cb = (char*)p.C + (int64_t)g.b * p.sC * 2;
-#pragma unroll
-    for (int j = 0; j < (CHUNKS + C::NT - 1) / C::NT; ++j) {
-        const int i = t + j * C::NT;
-        if (CHUNKS % C::NT != 0 && i >= CHUNKS)
-            break;
-        const int r = i / CPR, c = i % CPR;
-        const int m = g.m0 + r, n = g.n0 + c * 8;
-        if (m >= p.M || n >= p.N)
-            continue;
-        const u32x4 v = *(lds_u32x4*)(buf + (r * C::LDC + c * 8) * 2);
-        uint16_t* dst = (uint16_t*)Cb + (int64_t)m * p.N + n;
-        if (n + 8 <= p.N) {
-            *(u32x4_u*)dst = v;
-        } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (n + e < p.N)
-                    dst[e] = (uint16_t)elem16(v, e);
-        }
     }
 }
 

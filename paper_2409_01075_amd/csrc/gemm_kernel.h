@@ -37,6 +37,12 @@ typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 // unaligned mode, so these still compile to single 8/16-byte global accesses.
 typedef unsigned u32x4_u __attribute__((ext_vector_type(4), aligned(2)));
 typedef unsigned u32x2_u __attribute__((ext_vector_type(2), aligned(2)));
+// LDS pointers stay in address space 3 from the __shared__ object onwards, so
+// every LDS access compiles to a ds_* instruction with no generic-address
+// detour.
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 enum { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
 
@@ -72,6 +78,10 @@ struct Cfg {
     static constexpr int BV = H ? NB * KB / 8 / NT : KB * NB / 4 / NT;
     static constexpr int KI = H ? (MI == 16 ? 32 : 16) : (MI == 16 ? 4 : 2);   // K per MFMA
     static constexpr int KCH = H ? KI : (MI == 16 ? 16 : 8);                      // K per fragment load
+
+    // epilogue through LDS (store_lds) when the C tile fits the idle ring
+    static constexpr int LDC = NB + VE;
+    static constexpr bool LDS_EPI = MB * LDC * EB <= LDS_BYTES;
 
     static_assert(MB % WM == 0 && NB % WN == 0, "waves must tile the workgroup tile");
     static_assert(MW % MI == 0 && NW % MI == 0, "MFMA tiles must tile the wavefront tile");
@@ -559,14 +569,82 @@ __device__ __forceinline__ void store_direct(const VxGemmArgs& p, Acc<C>& acc, c
             }
 }
 
-// Split-K reduction, then the direct epilogue.
-template <class C>
-__device__ __forceinline__ void finish(const VxGemmArgs& p, Acc<C>& acc, const GridPos& g, int t, int lane,
-                                       int wm0, int wn0)
+// Four fp32 values -> four 16-bit outputs (round to nearest even), packed.
+template <int DT>
+__device__ __forceinline__ u32x2 pack4_16(float a0, float a1, float a2, float a3)
 {
-    if (p.split > 1 && !reduce_split<C>(p, acc, g, t))
-        return;
-    store_direct<C>(p, acc, g, lane, wm0, wn0);
+    unsigned h0, h1, h2, h3;
+    if (DT == DT_F16) {
+        h0 = __builtin_bit_cast(uint16_t, (_Float16)a0);
+        h1 = __builtin_bit_cast(uint16_t, (_Float16)a1);
+        h2 = __builtin_bit_cast(uint16_t, (_Float16)a2);
+        h3 = __builtin_bit_cast(uint16_t, (_Float16)a3);
+    } else {
+        h0 = __builtin_bit_cast(uint16_t, (__bf16)a0);
+        h1 = __builtin_bit_cast(uint16_t, (__bf16)a1);
+        h2 = __builtin_bit_cast(uint16_t, (__bf16)a2);
+        h3 = __builtin_bit_cast(uint16_t, (__bf16)a3);
+    }
+    return u32x2{pack2(h0, h1), pack2(h2, h3)};
+}
+
+// The epilogue through LDS.  The finished tile is written to the idle LDS
+// (converted to the output type, rows padded by 16 bytes against bank
+// conflicts), then leaves as 16-byte chunks of whole rows taken by
+// consecutive threads: a wave's store covers whole 128-byte lines instead of
+// 8 or 16 bytes in each of 16 or 32 rows.  Only the chunk that straddles the
+// N edge is stored element by element; rows of any alignment take misaligned
+// 16-byte stores.  Every wave must be done reading `buf` when this starts.
+template <class C>
+__device__ __forceinline__ void store_lds(const VxGemmArgs& p, Acc<C>& acc, const GridPos& g, int t, int lane, int wm0,
+                                          int wn0, lds_char* buf)
+{
+    constexpr int EB = C::EB, VE = 16 / EB, LDC = C::LDC;
+    static_assert(LDC * EB % 16 == 0, "16-byte aligned LDS rows");
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+            for (int gi = 0; gi < C::ACC / 4; ++gi) {
+                int dm, dn;
+                acc_coord<C::MI>(lane, gi, dm, dn);
+                const int r = wm0 + fm * C::MI + dm, c = wn0 + fn * C::MI + dn;
+                lds_char* dst = buf + (r * LDC + c) * EB;
+                const float a0 = acc.v[fn][fm][4 * gi], a1 = acc.v[fn][fm][4 * gi + 1];
+                const float a2 = acc.v[fn][fm][4 * gi + 2], a3 = acc.v[fn][fm][4 * gi + 3];
+                if constexpr (EB == 2)
+                    *(lds_u32x2*)dst = pack4_16<C::DT>(a0, a1, a2, a3);
+                else
+                    *(lds_u32x4*)dst = __builtin_bit_cast(u32x4, f32x4{a0, a1, a2, a3});
+            }
+    __syncthreads();
+    constexpr int CPR = C::NB / VE, CHUNKS = C::MB * CPR;
+    char* Cb = (char*)p.C + (int64_t)g.b * p.sC * EB;
+#pragma unroll
+    for (int j = 0; j < (CHUNKS + C::NT - 1) / C::NT; ++j) {
+        const int i = t + j * C::NT;
+        if (CHUNKS % C::NT != 0 && i >= CHUNKS)
+            break;
+        const int r = i / CPR, c = i % CPR;
+        const int m = g.m0 + r, n = g.n0 + c * VE;
+        if (m >= p.M || n >= p.N)
+            continue;
+        const u32x4 v = *(lds_u32x4*)(buf + (r * LDC + c * VE) * EB);
+        char* dst = Cb + ((int64_t)m * p.N + n) * EB;
+        if (n + VE <= p.N) {
+            *(u32x4_u*)dst = v;
+        } else {
+#pragma unroll
+            for (int e = 0; e < VE; ++e)
+                if (n + e < p.N) {
+                    if constexpr (EB == 2)
+                        ((uint16_t*)dst)[e] = (uint16_t)elem16(v, e);
+                    else
+                        ((unsigned*)dst)[e] = v[e];
+                }
+        }
+    }
 }
 
 // ------------------------------------------------- register-staged family --
@@ -605,7 +683,13 @@ __device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
             tl.store(smem + ((it + 1) & 1) * C::STAGE_BYTES, t);
         __syncthreads();
     }
-    finish<C>(p, acc, g, t, lane, wm0, wn0);
+    // the loop ends with a barrier: LDS is idle here
+    if (p.split > 1 && !reduce_split<C>(p, acc, g, t))
+        return;
+    if constexpr (C::LDS_EPI)
+        store_lds<C>(p, acc, g, t, lane, wm0, wn0, (lds_char*)smem);
+    else
+        store_direct<C>(p, acc, g, lane, wm0, wn0);
 }
 
 }  // namespace vxk
