@@ -32,6 +32,21 @@ def test_library_loads_and_exports_every_declared_symbol():
     assert set(names) <= exported, set(names) - exported
 
 
+def test_shipped_calibration_matches_the_built_kernels():
+    """The per-device table that ships beside the library was measured on
+    exactly the kernel set that is built: a stale table would silently turn
+    the hybrid analyzer back into the purely analytical one."""
+    path = os.path.join(os.path.dirname(vx.LIB_PATH), "calib_gfx950.txt")
+    assert os.path.exists(path)
+    kv = dict(ln.split(None, 1) for ln in open(path) if ln.strip() and not ln.startswith("#") and " " in ln)
+    assert kv["registry_hash"].strip() == vx.vx_registry_hash()
+    st, n = vx.vx_calibration_load(path)
+    try:
+        assert st == 0 and n == sum(vx.vx_registry_get(i).enabled for i in range(vx.vx_registry_count()))
+    finally:
+        vx.vx_calibration_load(None)
+
+
 def test_calibration_file_rules(tmp_path):
     """A calibration table is accepted only for this exact kernel set, and
     changes the cost model's answer; disabling it restores the analytical one."""
