@@ -48,6 +48,10 @@ struct DCfg {
     static constexpr int B_IPW = B_BYTES / WAVE_BYTES / NWAVE;
     static constexpr int LPS = A_IPW + B_IPW;
 
+    // With a ring of 3 or more stages the next K step's DMA is spread between
+    // the MFMA steps (a step of slack hides its latency); a 2-stage ring needs
+    // it issued whole right after the barrier, a full step before its use.
+    static constexpr bool SPREAD_DMA = STAGES >= 3;
     // epilogue through LDS (store_lds) when the C tile fits the idle ring
     static constexpr int LDC = NB + 8;
     static constexpr bool LDS_EPI = MB * LDC * 2 <= LDS_BYTES;
@@ -116,46 +120,74 @@ __device__ __forceinline__ void dma_lds(const u32x4& r, lds_char* dst, unsigned 
 {
     static_assert(LANE == 16, "16-byte chunks");
     const unsigned m0v = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)dst);
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m0v), "v"(voff), "s"(r)
+    // the resource is wave-uniform; readfirstlane keeps it in SGPRs whatever
+    // the compiler could prove about it (free when it is already scalar)
+    const u32x4 rs = {(unsigned)__builtin_amdgcn_readfirstlane(r[0]), (unsigned)__builtin_amdgcn_readfirstlane(r[1]),
+                      (unsigned)__builtin_amdgcn_readfirstlane(r[2]), (unsigned)__builtin_amdgcn_readfirstlane(r[3])};
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m0v), "v"(voff), "s"(rs)
                  : "memory");
 }
 
 template <class C>
 struct DmaTile {
-    // Issues the DMA of the K step starting at k0 into LDS stage `stage`.
-    __device__ __forceinline__ static void issue(lds_char* stage, const char* Apanel, const char* Bbatch, int k0, int kend,
-                                                 int Mrel, int n0, int N, int K, int wave, int lane)
+    // The DMA of one K step (starting at k0) into one LDS stage: LPS
+    // instructions per wave, A's A_IPW first, then B's B_IPW.  A step can be
+    // issued whole (issue) or one instruction at a time (one<I>), so that the
+    // main loop can spread it between the MFMAs of the step being computed.
+    lds_char* stage;
+    u32x4 ra, rb;   // A resource at column k0 of the panel; B resource at row k0, column n0
+    int kv, nv;     // valid columns of A from k0; valid columns of B from n0
+
+    __device__ __forceinline__ DmaTile(lds_char* stage_, const char* Apanel, const char* Bbatch, int k0, int kend, int n0,
+                                       int N)
+        : stage(stage_), ra(buffer_rsrc(Apanel + (int64_t)k0 * 2, kOOB)),
+          rb(buffer_rsrc(Bbatch + ((int64_t)k0 * N + n0) * 2, kOOB)), kv(kend - k0), nv(N - n0)
     {
-        // A: rows of the workgroup's panel; the resource starts at column k0
-        const u32x4 ra = buffer_rsrc(Apanel + (int64_t)k0 * 2, kOOB);
-        const int kv = kend - k0;   // valid columns from k0
-#pragma unroll
-        for (int i = 0; i < C::A_IPW; ++i) {
-            const int instr = wave * C::A_IPW + i;
-            lds_char* dst = stage + instr * C::WAVE_BYTES;
+    }
+
+    template <int I>
+    __device__ __forceinline__ void one(int Mrel, int N, int K, int wave, int lane) const
+    {
+        if constexpr (I < C::A_IPW) {
+            // A: rows of the workgroup's panel
+            const int instr = wave * C::A_IPW + I;
             const int slot = instr * 64 + lane;                  // chunk index in the stage
             const int r = slot / C::CPA, c = (slot % C::CPA) ^ swz_a(r, C::SWA);
             const bool ok = r < Mrel && c * 8 < kv;
-            dma_lds<C::LANE_BYTES>(ra, dst, ok ? (unsigned)((r * K + c * 8) * 2) : kOOB);
-        }
-        // B: rows k0.. of the batch's B, columns from n0
-        const u32x4 rb = buffer_rsrc(Bbatch + ((int64_t)k0 * N + n0) * 2, kOOB);
-        const int nv = N - n0;      // valid columns from n0
-#pragma unroll
-        for (int i = 0; i < C::B_IPW; ++i) {
-            const int instr = wave * C::B_IPW + i;
-            lds_char* dst = stage + C::A_BYTES + instr * C::WAVE_BYTES;
+            dma_lds<C::LANE_BYTES>(ra, stage + instr * C::WAVE_BYTES, ok ? (unsigned)((r * K + c * 8) * 2) : kOOB);
+        } else {
+            // B: rows k0.. of the batch's B, columns from n0
+            const int instr = wave * C::B_IPW + (I - C::A_IPW);
             const int slot = instr * 64 + lane;
             const int k = slot / C::CPB, c = (slot % C::CPB) ^ swz_b<C::CPB>(k);
             const bool ok = k < kv && c * 8 < nv;
-            dma_lds<C::LANE_BYTES>(rb, dst, ok ? (unsigned)((k * N + c * 8) * 2) : kOOB);
+            dma_lds<C::LANE_BYTES>(rb, stage + C::A_BYTES + instr * C::WAVE_BYTES,
+                                   ok ? (unsigned)((k * N + c * 8) * 2) : kOOB);
         }
+    }
+
+    // instructions [FIRST, LAST) of the step
+    template <int FIRST, int LAST>
+    __device__ __forceinline__ void range(int Mrel, int N, int K, int wave, int lane) const
+    {
+        if constexpr (FIRST < LAST) {
+            one<FIRST>(Mrel, N, K, wave, lane);
+            range<FIRST + 1, LAST>(Mrel, N, K, wave, lane);
+        }
+    }
+
+    __device__ __forceinline__ void issue(int Mrel, int N, int K, int wave, int lane) const
+    {
+        range<0, C::LPS>(Mrel, N, K, wave, lane);
     }
 };
 
-// Level 0 over one LDS stage.
+// Level 0 over one LDS stage.  The fragments of MFMA step kk+1 are read from
+// LDS while the MFMAs of step kk run (two register sets), so the LDS latency
+// and transfer overlap the matrix-core work instead of preceding it.
 template <class C>
-__device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm0, int wn0, int lane)
+__device__ __forceinline__ void dma_frags(lds_char* stage, u32x4 (&fa)[C::FM], u32x4 (&fb)[C::FN], int kk, int wm0, int wn0,
+                                          int lane)
 {
     lds_char* As = stage;
     lds_char* Bs = stage + C::A_BYTES;
@@ -165,35 +197,82 @@ __device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm
     const int tr_n = (C::MI == 16 ? 0 : 16 * (grp & 1)) + 4 * (s & 3);
     const int tr_k = (C::MI == 16 ? 8 * grp : 8 * (grp >> 1)) + (s >> 2);
 #pragma unroll
-    for (int kk = 0; kk < C::KB / C::KI; ++kk) {
-        u32x4 fa[C::FM], fb[C::FN];
+    for (int fm = 0; fm < C::FM; ++fm) {
+        const int m = wm0 + fm * C::MI + li;
+        const int c = (kk * (C::KI / 8) + lg) ^ swz_a(m, C::SWA);
+        fa[fm] = *(lds_u32x4*)(As + m * (C::KB * 2) + c * 16);
+    }
 #pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm) {
-            const int m = wm0 + fm * C::MI + li;
-            const int c = (kk * (C::KI / 8) + lg) ^ swz_a(m, C::SWA);
-            fa[fm] = *(lds_u32x4*)(As + m * (C::KB * 2) + c * 16);
-        }
-#pragma unroll
-        for (int fn = 0; fn < C::FN; ++fn) {
-            const int n = wn0 + fn * C::MI + tr_n;
-            const int k1 = kk * C::KI + tr_k, k2 = k1 + 4;
-            lds_char* p1 = Bs + k1 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k1)) << 4) + (n & 7) * 2;
-            lds_char* p2 = Bs + k2 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k2)) << 4) + (n & 7) * 2;
-            const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p1);
-            const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p2);
-            const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-            fb[fn] = u32x4{l2[0], l2[1], h2[0], h2[1]};
+    for (int fn = 0; fn < C::FN; ++fn) {
+        const int n = wn0 + fn * C::MI + tr_n;
+        const int k1 = kk * C::KI + tr_k, k2 = k1 + 4;
+        lds_char* p1 = Bs + k1 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k1)) << 4) + (n & 7) * 2;
+        lds_char* p2 = Bs + k2 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k2)) << 4) + (n & 7) * 2;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p1);
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p2);
+        const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+        fb[fn] = u32x4{l2[0], l2[1], h2[0], h2[1]};
+    }
+}
+
+// The MFMAs of one LDS stage; when `on`, the DMA `next` of a later K step is
+// issued too: whole before the first MFMAs (2-stage rings), or in NKK parts,
+// one after the MFMAs of each MFMA step (deeper rings), so that the CU's load
+// path fills the ring while the matrix cores run.
+template <int NKK, int KK, class C>
+__device__ __forceinline__ void dma_part(const DmaTile<C>& next, bool on, int Mrel, int N, int K, int wave, int lane)
+{
+    constexpr int NP = C::SPREAD_DMA ? NKK : 1;   // MFMA steps the DMA is spread over
+    constexpr int PER = (C::LPS + NP - 1) / NP;
+    constexpr int FIRST = KK * PER < C::LPS ? KK * PER : C::LPS;
+    constexpr int LAST = (KK + 1) * PER < C::LPS ? (KK + 1) * PER : C::LPS;
+    if constexpr (FIRST < LAST) {
+        if (on)
+            next.template range<FIRST, LAST>(Mrel, N, K, wave, lane);
+    }
+}
+
+template <class C, int KK = 0>
+__device__ __forceinline__ void dma_steps(lds_char* stage, Acc<C>& acc, u32x4 (&fa)[2][C::FM], u32x4 (&fb)[2][C::FN], int wm0,
+                                          int wn0, int lane, const DmaTile<C>& next, bool on, int Mrel, int N, int K,
+                                          int wave)
+{
+    constexpr int NKK = C::KB / C::KI;
+    if constexpr (KK < NKK) {
+        if constexpr (KK + 1 < NKK)
+            dma_frags<C>(stage, fa[(KK + 1) & 1], fb[(KK + 1) & 1], KK + 1, wm0, wn0, lane);
+        // keep the reads of step KK+1 ahead of the MFMAs of step KK (the
+        // machine scheduler would otherwise sink each read next to its use)
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (!C::SPREAD_DMA) {
+            dma_part<NKK, KK, C>(next, on, Mrel, N, K, wave, lane);
+            __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm) {
                 if constexpr (C::MI == 16)
-                    mfma16<C::DT, 16>(fb[fn], fa[fm], acc.v[fn][fm]);
+                    mfma16<C::DT, 16>(fb[KK & 1][fn], fa[KK & 1][fm], acc.v[fn][fm]);
                 else
-                    mfma32<C::DT>(fb[fn], fa[fm], acc.v[fn][fm]);
+                    mfma32<C::DT>(fb[KK & 1][fn], fa[KK & 1][fm], acc.v[fn][fm]);
             }
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (C::SPREAD_DMA) {
+            dma_part<NKK, KK, C>(next, on, Mrel, N, K, wave, lane);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        dma_steps<C, KK + 1>(stage, acc, fa, fb, wm0, wn0, lane, next, on, Mrel, N, K, wave);
     }
+}
+
+template <class C>
+__device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm0, int wn0, int lane, const DmaTile<C>& next,
+                                            bool on, int Mrel, int N, int K, int wave)
+{
+    u32x4 fa[2][C::FM], fb[2][C::FN];
+    dma_frags<C>(stage, fa[0], fb[0], 0, wm0, wn0, lane);
+    dma_steps<C>(stage, acc, fa, fb, wm0, wn0, lane, next, on, Mrel, N, K, wave);
 }
 
 template <class C>
@@ -227,7 +306,8 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s)
         if (s < g.nk)
-            DmaTile<C>::issue(VX_STAGE(s), Apanel, Bbatch, g.kbeg + s * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
+            DmaTile<C>(VX_STAGE(s), Apanel, Bbatch, g.kbeg + s * C::KB, g.kend, g.n0, p.N).issue(Mrel, p.N, p.K, wave,
+                                                                                                   lane);
     // main loop, unrolled by STAGES so that every stage index is a constant
     for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
 #pragma unroll
@@ -237,10 +317,10 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
                 break;
             wait_steps<C::LPS, C::STAGES - 2>(g.nk - 1 - it);   // step `it` has landed (this wave's part)
             __builtin_amdgcn_s_barrier();                      // ... and every wave's; stage it-1 is free
-            if (it + C::STAGES - 1 < g.nk)
-                DmaTile<C>::issue(VX_STAGE((j + C::STAGES - 1) % C::STAGES), Apanel, Bbatch,
-                                  g.kbeg + (it + C::STAGES - 1) * C::KB, g.kend, Mrel, g.n0, p.N, p.K, wave, lane);
-            dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane);
+            // step it+STAGES-1 goes into the freed stage, issued between the MFMAs of step it
+            const DmaTile<C> next(VX_STAGE((j + C::STAGES - 1) % C::STAGES), Apanel, Bbatch,
+                                  g.kbeg + (it + C::STAGES - 1) * C::KB, g.kend, g.n0, p.N);
+            dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, next, it + C::STAGES - 1 < g.nk, Mrel, p.N, p.K, wave);
         }
     }
     wait_vm<0>();   // nothing is in flight here; kept as a guard before LDS is released
