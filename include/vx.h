@@ -84,15 +84,20 @@ typedef struct vx_kernel_info {
     vx_dtype dtype;
     int mb, nb, kb;                /* workgroup tile */
     int wm, wn;                    /* wavefront grid; wavefront tile = (mb/wm) x (nb/wn) */
-    int mfma_m, mfma_n, mfma_k;    /* instruction tile */
+    int mfma_m, mfma_n, mfma_k;    /* instruction tile (0 for the vector-ALU family) */
     int vec;                       /* 1: needs 16-byte-aligned operand rows; 0: any element alignment */
-    int family;                    /* 0: loads staged through registers, 1: direct-to-LDS DMA */
-    int stages;                    /* LDS ring depth (K steps in flight + 1) */
+    int family;                    /* 0: MFMA, loads staged through registers; 1: MFMA, direct-to-LDS
+                                      DMA; 2: vector ALU (v_dot2 / v_fma), B rows straight to VGPRs,
+                                      for small M (mb = the rows one workgroup covers) */
+    int stages;                    /* families 0, 1: LDS ring depth (K steps in flight + 1);
+                                      family 2: K groups per lane per register set */
     int threads;
     int lds_bytes;
     int vgprs, agprs, sgprs;       /* from the compiler's resource report of this build */
     int scratch_bytes;             /* per lane; 0 for every enabled kernel */
     int enabled;
+    int k_max;                     /* longest K slice one workgroup takes (0: unbounded); family 2
+                                      keeps its slice of A in LDS */
 } vx_kernel_info;
 
 /* A concrete execution plan for one call. */

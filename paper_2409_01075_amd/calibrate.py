@@ -7,10 +7,11 @@ kernel itself on synthetic shapes built from its own workgroup tile and the
 device's CU count - never from application shapes:
 
   * "full": one wave of workgroups filling the device (CUs x resident
-    workgroups per CU), with 2 and with 10 K steps per workgroup;
+    workgroups per CU), with 2 and with 10 K steps per workgroup (fewer for
+    a kernel whose K slice is bounded);
   * "light": 32 workgroups (or fewer if the device holds fewer), same K steps.
 
-Each pair gives the time of one workgroup K step (difference over 8 steps) and
+Each pair gives the time of one workgroup K step (difference over the extra steps) and
 the fixed per-call cost (the remainder, less the launch floor).  With the
 device full, the kernel also runs split-K with 2 and 4 slices of 2 steps each:
 the extra time over the unsplit 2-step call gives the split-K epilogue cost
@@ -114,18 +115,21 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
             finally:
                 vx.vx_force_plan(-1, 0)
 
+        # K steps per workgroup: 2 and 10, or as many as the kernel's longest
+        # slice allows (kernels that hold their slice of A in LDS)
+        nk_hi = 10 if k.k_max <= 0 else max(3, min(10, k.k_max // k.kb))
         for tag, G in (("full", slots), ("light", min(32, slots))):
             nt = min(16, G)
             mt = G // nt
-            for nk in (2, 10):
+            for nk in (2, nk_hi):
                 meas[(tag, nk)] = timed(mt * k.mb, nt * k.nb, nk * k.kb, 1)
         for s_ in (2, 4):
             tiles = max(1, slots // s_)
             nt = min(16, tiles)
             mt = max(1, tiles // nt)
             meas[("split", s_)] = timed(mt * k.mb, nt * k.nb, s_ * 2 * k.kb, s_)
-        step_full = max((meas[("full", 10)] - meas[("full", 2)]) / 8.0, 1.0)
-        step_light = max((meas[("light", 10)] - meas[("light", 2)]) / 8.0, 1.0)
+        step_full = max((meas[("full", nk_hi)] - meas[("full", 2)]) / (nk_hi - 2.0), 1.0)
+        step_light = max((meas[("light", nk_hi)] - meas[("light", 2)]) / (nk_hi - 2.0), 1.0)
         fix_full = max(meas[("full", 2)] - 2 * step_full - launch, 0.0)
         fix_light = max(meas[("light", 2)] - 2 * step_light - launch, 0.0)
         load_light = min(32, slots) / float(slots)

@@ -235,7 +235,42 @@ def _entry(dtype, family, stages, c, vec, hw):
     mb, nb, kb, wm, wn, mi = c
     lds = lds_bytes_dma(mb, nb, kb, stages) if family == "dma" else lds_bytes(dtype, mb, nb, kb)
     return dict(dtype=dtype, dt=DT_CODE[dtype], family=family, stages=stages, mb=mb, nb=nb, kb=kb, wm=wm,
-                wn=wn, mi=mi, vec=vec, threads=wm * wn * hw["wave"], lds=lds)
+                wn=wn, mi=mi, vec=vec, threads=wm * wn * hw["wave"], lds=lds, k_max=0)
+
+
+# ------------------------------------------------- vector-ALU family (L0') --
+# The adaptive second backend for small M (the paper's CUDA-core path next to
+# the tensor-core path): level 0 is one lane's MT x VE outputs computed with
+# v_dot2 (16-bit, on pairs of k) or v_fma (fp32) instead of an MFMA tile.
+# One 16-byte chunk per lane of a B row, 8 lanes per 128-byte row segment:
+# NB = 8 chunks; 8 k groups per wave; U groups per lane per register set.
+VALU_ROWS = (4, 8, 16)
+VALU_WAVES = (4, 8)
+VALU_U = (2, 4)
+VALU_A_LDS = 128 * 1024     # the A slice held in LDS
+
+
+def valu_candidates(dtype, hw=GFX950):
+    eb = ELEM_BYTES[dtype]
+    ve = 16 // eb
+    nb = 8 * ve
+    pk = 2 if eb == 2 else 1
+    out = []
+    for mt in VALU_ROWS:
+        for waves in VALU_WAVES:
+            for u in VALU_U:
+                kpi = waves * 8 * pk * u
+                kmax = min(8192, VALU_A_LDS // (mt * eb)) // kpi * kpi
+                red = waves * mt * nb * 4
+                lds = max(kmax * mt * eb, red)
+                # accumulators mt x ve, two register sets of u x pk chunks: within 512 VGPRs per lane
+                # for one wave per SIMD, 256 for two
+                regs = mt * ve + 2 * u * pk * 4 + mt + ve + 24
+                if regs > (512 if waves <= 4 else 256) or kmax < kpi or lds > hw["lds_bytes"] - LDS_RESERVE:
+                    continue
+                out.append(dict(dtype=dtype, dt=DT_CODE[dtype], family="valu", stages=u, mb=mt, nb=nb, kb=kpi, wm=1,
+                                wn=waves, mi=0, vec=1, threads=waves * hw["wave"], lds=lds, k_max=kmax))
+    return out
 
 
 def registry(hw=GFX950):
@@ -261,6 +296,8 @@ def registry(hw=GFX950):
     for c in generate_candidates_for_layer(2, "f32", hw, "reg")[0]:
         for vec in (1, 0):
             out.append(_entry("f32", "reg", 2, c, vec, hw))
+    for dtype in ("f16", "bf16", "f32"):
+        out += valu_candidates(dtype, hw)
     for i, e in enumerate(out):
         e["id"] = i
     return out

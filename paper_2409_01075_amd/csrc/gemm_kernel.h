@@ -458,40 +458,31 @@ __device__ __forceinline__ void acc_zero(Acc<C>& acc)
 }
 
 // ------------------------------------------------------------ Store_Func ---
-// Split-K reduction (when the launch splits K): returns false for a slice that
-// is not the last to arrive at its tile (it has nothing more to do), true for
-// the workgroup that now holds the tile's full sum and writes C.  The result
-// is uniform over the workgroup.
-template <class C>
-__device__ __forceinline__ bool reduce_split(const VxGemmArgs& p, Acc<C>& acc, const GridPos& g, int t)
+// Split-K reduction of one output tile whose fp32 values are held by the first
+// `nact` threads of the workgroup, V groups of 4 per thread.  Each slice
+// publishes its partial tile, then the last slice to arrive sums all slices
+// in order 0..split-1.  Returns false for a slice that is not the last to
+// arrive (it has nothing more to do), true for the workgroup that now holds
+// the tile's full sum in v.  The result is uniform over the workgroup.
+// Partials move as 16-byte device-coherent (sc1) buffer stores and loads,
+// laid out [slice][group of 4][thread] so each wave instruction covers 1 KiB
+// contiguously; no workgroup has to write back or invalidate a whole L2.
+template <int V>
+__device__ __forceinline__ bool split_reduce(const VxGemmArgs& p, const GridPos& g, f32x4 (&v)[V], int t, int nact)
 {
-    // Split-K: publish this slice's fp32 partial tile, then the last slice
-    // to arrive sums all slices in order 0..split-1 and writes C.
-    // Partials move as 16-byte device-coherent (sc1) buffer stores and
-    // loads, laid out [slice][group of 4 accumulators][thread] so each
-    // wave instruction covers 1 KiB contiguously; no workgroup has to
-    // write back or invalidate a whole L2.
-    constexpr int PER = C::FN * C::FM * C::ACC;       // floats per thread
-    constexpr int P4 = PER / 4;
-    constexpr unsigned SLICE_BYTES = (unsigned)PER * C::NT * 4;   // = Mb * Nb * 4
+    const unsigned SLICE_BYTES = (unsigned)V * (unsigned)nact * 16u;
     const int64_t tile_id = (int64_t)g.b * g.tiles + g.tm * p.tiles_n + g.tn;
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.ws + tile_id * (int64_t)p.split * (PER * C::NT)), (short)0, (int)(SLICE_BYTES * p.split),
-        0x00020000);
+        (void*)(p.ws + tile_id * (int64_t)p.split * (V * nact * 4)), (short)0, (int)(SLICE_BYTES * p.split), 0x00020000);
     constexpr int SC1 = 16;   // cache policy: device scope
+    const bool act = t < nact;
     const unsigned mine = (unsigned)g.z * SLICE_BYTES;
+    if (act) {
 #pragma unroll
-    for (int fn = 0; fn < C::FN; ++fn)
-#pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm)
-#pragma unroll
-            for (int gi = 0; gi < C::ACC / 4; ++gi) {
-                const int e4 = (fn * C::FM + fm) * (C::ACC / 4) + gi;
-                const f32x4 part = {acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1], acc.v[fn][fm][4 * gi + 2],
-                                    acc.v[fn][fm][4 * gi + 3]};
-                const u32x4 v = __builtin_bit_cast(u32x4, part);
-                __builtin_amdgcn_raw_buffer_store_b128(v, rw, mine + (unsigned)(e4 * C::NT + t) * 16, 0, SC1);
-            }
+        for (int e4 = 0; e4 < V; ++e4)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v[e4]), rw,
+                                                   mine + (unsigned)(e4 * nact + t) * 16, 0, SC1);
+    }
     // every store of the partial tile has completed before the arrival is counted
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
@@ -501,33 +492,62 @@ __device__ __forceinline__ bool reduce_split(const VxGemmArgs& p, Acc<C>& acc, c
     __syncthreads();
     if (arrived != (unsigned)(p.split - 1))
         return false;
-    static_assert(PER % 4 == 0, "accumulators come in groups of 4");
     // Sum slices 0..split-1 in order.  The loads of SF slices are issued
     // together before any of them is added, so the reduction waits for one
     // memory round trip per SF slices rather than one per slice (the last
     // slice's own partial is read back like the others: it is complete).
-    constexpr int SF = P4 <= 2 ? 8 : P4 <= 4 ? 4 : P4 <= 8 ? 2 : 1;
-    f32x4 sum[P4];
-    for (int zz0 = 0; zz0 < p.split; zz0 += SF) {
-        f32x4 part[SF][P4];
+    if (act) {
+        constexpr int SF = V <= 2 ? 8 : V <= 4 ? 4 : V <= 8 ? 2 : 1;
+        f32x4 sum[V];
+        for (int zz0 = 0; zz0 < p.split; zz0 += SF) {
+            f32x4 part[SF][V];
 #pragma unroll
-        for (int j = 0; j < SF; ++j) {
-            const int zz = min(zz0 + j, p.split - 1);   // in range; surplus loads are not added
+            for (int j = 0; j < SF; ++j) {
+                const int zz = min(zz0 + j, p.split - 1);   // in range; surplus loads are not added
 #pragma unroll
-            for (int e4 = 0; e4 < P4; ++e4)
-                part[j][e4] = __builtin_bit_cast(
-                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, zz * SLICE_BYTES + (unsigned)(e4 * C::NT + t) * 16,
-                                                                 0, SC1));
+                for (int e4 = 0; e4 < V; ++e4)
+                    part[j][e4] = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, zz * SLICE_BYTES + (unsigned)(e4 * nact + t) * 16,
+                                                                     0, SC1));
+            }
+#pragma unroll
+            for (int j = 0; j < SF; ++j) {
+                if (zz0 + j >= p.split)
+                    break;
+#pragma unroll
+                for (int e4 = 0; e4 < V; ++e4)
+                    sum[e4] = zz0 + j == 0 ? part[j][e4] : sum[e4] + part[j][e4];
+            }
         }
 #pragma unroll
-        for (int j = 0; j < SF; ++j) {
-            if (zz0 + j >= p.split)
-                break;
-#pragma unroll
-            for (int e4 = 0; e4 < P4; ++e4)
-                sum[e4] = zz0 + j == 0 ? part[j][e4] : sum[e4] + part[j][e4];
-        }
+        for (int e4 = 0; e4 < V; ++e4)
+            v[e4] = sum[e4];
     }
+    if (t == 0)
+        __hip_atomic_store(&p.tickets[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+}
+
+// Split-K reduction of the MFMA accumulators (every thread holds
+// FN x FM x ACC values, in groups of 4 along the accumulator index).
+template <class C>
+__device__ __forceinline__ bool reduce_split(const VxGemmArgs& p, Acc<C>& acc, const GridPos& g, int t)
+{
+    constexpr int P4 = C::FN * C::FM * C::ACC / 4;
+    static_assert(C::ACC % 4 == 0, "accumulators come in groups of 4");
+    f32x4 v[P4];
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+            for (int gi = 0; gi < C::ACC / 4; ++gi) {
+                const int e4 = (fn * C::FM + fm) * (C::ACC / 4) + gi;
+                v[e4] = f32x4{acc.v[fn][fm][4 * gi], acc.v[fn][fm][4 * gi + 1], acc.v[fn][fm][4 * gi + 2],
+                              acc.v[fn][fm][4 * gi + 3]};
+            }
+    if (!split_reduce<P4>(p, g, v, t, C::NT))
+        return false;
 #pragma unroll
     for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
@@ -537,10 +557,8 @@ __device__ __forceinline__ bool reduce_split(const VxGemmArgs& p, Acc<C>& acc, c
                 const int e4 = (fn * C::FM + fm) * (C::ACC / 4) + gi;
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    acc.v[fn][fm][4 * gi + e] = sum[e4][e];
+                    acc.v[fn][fm][4 * gi + e] = v[e4][e];
             }
-    if (t == 0)
-        __hip_atomic_store(&p.tickets[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return true;
 }
 

@@ -91,6 +91,8 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     }
     if (kps > INT32_MAX || tiles > INT32_MAX)
         return -1.0;
+    if (k.k_max > 0 && kps > k.k_max)   // the kernel holds a whole slice of A in LDS
+        return -1.0;
     const int64_t units = tiles * split;
     if (units > INT32_MAX)
         return -1.0;
@@ -106,6 +108,11 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
         if ((double)k.mb * sh.K * eb >= 2147483648.0 || (double)k.kb * sh.N * eb >= 2147483648.0)
             return -1.0;
     }
+    if (k.family == 2) {
+        // the vector-ALU kernels address a whole slice of B with 32-bit offsets
+        if ((double)kps * sh.N * eb >= 2147483648.0)
+            return -1.0;
+    }
     if (k_per_split)
         *k_per_split = (int)kps;
 
@@ -118,15 +125,21 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     const int64_t active = std::min(units, slots);
     const double per_cu = (double)cdiv(active, hw.num_cu);
 
-    // Level 0: one K step of MFMAs fed from LDS (Eq. 2 over the Kb/k0 sub-steps).
-    const double flop_clk = sh.dt == VX_F32 ? hw.mfma_flop_clk_cu_f32 : hw.mfma_flop_clk_cu_f16;
+    // Level 0: one K step of MFMAs fed from LDS (Eq. 2 over the Kb/k0 sub-steps),
+    // or of vector-ALU dot products on B chunks held in registers (family 2:
+    // v_dot2 retires 4 FLOP per lane, v_fma 2, one wave instruction per SIMD
+    // every 4 clocks; A comes from LDS at a few bytes per k).
+    const bool valu = k.family == 2;
+    const double flop_clk = valu ? 64.0 * hw.simd_per_cu * (sh.dt == VX_F32 ? 0.5 : 1.0)
+                                 : (sh.dt == VX_F32 ? hw.mfma_flop_clk_cu_f32 : hw.mfma_flop_clk_cu_f16);
     const double rate_wg = flop_clk * hw.clock_ghz *
                            std::min((double)waves / hw.simd_per_cu, 1.0 / per_cu);   // FLOP/ns
-    const int kstep = k.mfma_k * (sh.dt == VX_F32 ? 4 : 1);  // fp32 loads 4 MFMA steps at once
+    const int kstep = valu ? k.kb : k.mfma_k * (sh.dt == VX_F32 ? 4 : 1);  // fp32 loads 4 MFMA steps at once
     const int64_t sub = std::max<int64_t>(1, k.kb / kstep);
     const double c_mfma = 2.0 * k.mb * k.nb * kstep / rate_wg;
     const double lds_bw = hw.lds_bytes_clk_cu * hw.clock_ghz / per_cu;             // B/ns
-    const double t_lds = (double)waves * ((double)k.mb / k.wm + (double)k.nb / k.wn) * kstep * eb / lds_bw;
+    const double t_lds = valu ? (double)k.threads * k.stages * k.mb * 4.0 / lds_bw
+                              : (double)waves * ((double)k.mb / k.wm + (double)k.nb / k.wn) * kstep * eb / lds_bw;
     const double cost0 = vx_cost_temporal(t_lds, sub, c_mfma, 0.0);
 
     // Level 1: the K loop of one workgroup (Eq. 2 over n_k K steps).
@@ -135,14 +148,15 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     // straddle an extra cache line per row segment and the ragged edge chunks
     // are gathered element by element
     const double load_factor = k.vec ? 1.0 : 1.25;
-    const double xfer = (double)(k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
+    // (family 2 reads only B from memory in the loop; its A slice is loaded once)
+    const double xfer = (double)(valu ? k.nb : k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
     const double t_load = hw.mem_latency_ns + xfer;
     double t_store = (double)k.mb * k.nb * eb / bw_wg;
     if (split > 1) {
         const double part = (double)k.mb * k.nb * 4.0 / bw_wg;
         t_store += part + hw.atomic_latency_ns + hw.mem_latency_ns + (double)(split - 1) * part;
     }
-    const int depth = std::max(1, k.stages - 1);
+    const int depth = valu ? 1 : std::max(1, k.stages - 1);   // family 2: two register sets
     double t1;
     if (depth == 1 || nk <= 1) {
         t1 = vx_cost_temporal(t_load, nk, cost0, t_store);

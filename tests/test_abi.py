@@ -152,9 +152,22 @@ def test_registry_invariants():
     assert n > 0
     isa = {0: {(16, 16, 4), (32, 32, 2)}, 1: {(16, 16, 32), (32, 32, 16)}, 2: {(16, 16, 32), (32, 32, 16)}}
     seen = set()
+    valu = 0
     for i in range(n):
         k = vx.vx_registry_get(i)
         assert k.id == i
+        if k.family == 2:
+            # vector-ALU backend: one wave covers 8 column chunks of 16 bytes x 8 k groups,
+            # Kb = waves x 8 groups x (2 rows per dot2 pair for 16-bit) x groups per lane
+            valu += 1
+            eb = 4 if k.dtype == 0 else 2
+            assert (k.mfma_m, k.mfma_n, k.mfma_k) == (0, 0, 0) and k.wm == 1 and k.vec == 1
+            assert k.nb == 8 * (16 // eb) and k.mb in (4, 8, 16)
+            assert k.kb == k.wn * 8 * (2 if eb == 2 else 1) * k.stages
+            assert k.k_max > 0 and k.k_max % k.kb == 0 and k.k_max * k.mb * eb <= k.lds_bytes <= 160 * 1024
+            assert k.threads == 64 * k.wn and k.enabled == (1 if k.scratch_bytes == 0 else 0)
+            continue
+        assert k.k_max == 0
         assert (k.mfma_m, k.mfma_n, k.mfma_k) in isa[k.dtype]                  # L0: FilterByISA
         mw, nw = k.mb // k.wm, k.nb // k.wn
         assert k.mb == k.wm * mw and k.nb == k.wn * nw                          # L2 multiple of L1
@@ -166,6 +179,7 @@ def test_registry_invariants():
         assert k.vgprs + k.agprs <= 512 and k.vgprs > 0
         seen.add((k.dtype, k.vec))
     assert seen == {(d, v) for d in (0, 1, 2) for v in (0, 1)}
+    assert valu > 0
     enabled = sum(vx.vx_registry_get(i).enabled for i in range(n))
     assert enabled >= 0.9 * n
 

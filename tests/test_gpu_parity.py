@@ -196,6 +196,28 @@ def test_every_ring_kernel_long_k(code):
 
 
 @pytest.mark.parametrize("code", DTS)
+def test_vector_alu_kernels_random_within_bound(code):
+    """Every kernel of the vector-ALU family on random inputs: ragged M (below
+    and above one tile's rows), a partial N tile, a K that ends inside a step;
+    unsplit and with 3 K slices."""
+    g = I.rng(470 + code)
+    ran = 0
+    for k in _kernel_cases():
+        if k.dtype != code or not k.enabled or k.family != 2:
+            continue
+        for (M, N, K, split) in ((1, 200, 1000, 1), (k.mb + 3, 72, 3 * k.kb + 24, 3)):
+            A = I.normal(g, (M, K), code)
+            B = I.normal(g, (K, N), code, 0.02)
+            assert vx.vx_force_plan(k.id, split) == 0
+            C = run_gemm(A, B, code)
+            vx.vx_force_plan(-1, 0)
+            ref, mag = oracle.gemm(A, B, code)
+            tolerance.check(C, ref, mag, code, "vector-ALU kernel %d M %d split %d" % (k.id, M, split))
+        ran += 1
+    assert ran > 0
+
+
+@pytest.mark.parametrize("code", DTS)
 @pytest.mark.parametrize("split", [2, 3, 5, 8])
 def test_split_k_integer_exact(code, split):
     g = I.rng(500 + 10 * code + split)
