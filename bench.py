@@ -46,6 +46,9 @@ def _parse():
                     choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single", "mixed"],
                     help="sweep (default, the headline metric) or one of the other GEMM sets")
     ap.add_argument("--trials", type=int, default=None, help="trials of a GEMM set (default: the full set)")
+    ap.add_argument("--adapt", action="store_true",
+                    help="hardware-adaptation study (Section 7.4): fp16, N in {1024, 2048, 4096}, K = 1024, "
+                         "M = 1..16, with the matrix-core kernels only, the vector-ALU kernels only, and both")
     ap.add_argument("--study", action="store_true",
                     help="selector quality study: time every feasible (kernel, split) plan of each GEMM "
                          "of the set and compare the selector's pick, and the Static1/Static2 hierarchy "
@@ -376,6 +379,70 @@ def run_study(args):
     print(json.dumps(out), flush=True)
 
 
+def run_adapt(args):
+    """The paper's dynamic hardware adaptation experiment (Section 7.4): the
+    same GEMMs planned three ways -- matrix-core kernels only, vector-ALU
+    kernels only, and the adaptive default (the calibrated argmin over both) --
+    each timed over rotating HBM-resident operands.  Reports every time and the
+    largest gain of the adaptive setting over each fixed one."""
+    import numpy as np
+    import torch
+    from paper_2409_01075_amd import inputs as I
+    from paper_2409_01075_amd import vx
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = vx.lib()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    torch.cuda._sleep(1000000)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    spin = int(1e6 / max(e0.elapsed_time(e1), 1e-3) * 0.3)
+    K = 1024
+    settings = (("matrix-core only", vx.BACKEND_MFMA), ("vector-ALU only", vx.BACKEND_VALU), ("adaptive", 0))
+    rows = []
+    try:
+        for N in (1024, 2048, 4096):
+            for M in range(1, 17):
+                def mk(dev, M=M, N=N):
+                    g = I.rng(7000 + 100 * M + N // 1024)
+                    A = I.uniform(g, (M, K), 1)
+                    B = I.uniform(g, (K, N), 1)
+                    return (torch.from_numpy(A.view("int16")).to(dev).view(torch.float16),
+                            torch.from_numpy(B.view("int16")).to(dev).view(torch.float16))
+                call, R, keep = _study_ctx(("M=%d N=%d" % (M, N), 1, M, N, K, 1, mk), dev, args.rot_mib, L, sp)
+                r = {"M": M, "N": N, "K": K}
+                for name, mask in settings:
+                    if vx.vx_restrict_backends(mask) != 0:
+                        raise RuntimeError("vx_restrict_backends(%d)" % mask)
+                    p = vx.vx_plan_query(1, M, N, K, vx.VX_F16)
+                    call(0)
+                    r[name] = _time_calls(call, R, stream, spin) * 1e6
+                    r[name + " kernel"] = [p.kernel_id, p.kernel.family, p.split_k]
+                del keep, call
+                rows.append(r)
+                print("N=%4d M=%2d  matrix-core %6.2f us  vector-ALU %6.2f us  adaptive %6.2f us (family %d)"
+                      % (N, M, r["matrix-core only"], r["vector-ALU only"], r["adaptive"], r["adaptive kernel"][1]),
+                      file=sys.stderr, flush=True)
+    finally:
+        vx.vx_restrict_backends(0)
+    gain_mfma = max(r["matrix-core only"] / r["adaptive"] - 1.0 for r in rows)
+    gain_valu = max(r["vector-ALU only"] / r["adaptive"] - 1.0 for r in rows)
+    geo = lambda v: float(np.exp(np.mean(np.log(v))))
+    out = {"study": "hardware adaptation", "dtype": "f16", "K": K, "N": [1024, 2048, 4096], "M": "1..16",
+           "adaptive_max_gain_over_matrix_core_only": gain_mfma,
+           "adaptive_max_gain_over_vector_alu_only": gain_valu,
+           "geomean_us": {name: geo([r[name] for r in rows]) for name, _ in settings},
+           "adaptive_picks_vector_alu": sum(1 for r in rows if r["adaptive kernel"][1] == 2),
+           "gemms": len(rows), "selector": _selector_kind()}
+    if args.detail:
+        with open(args.detail, "w") as f:
+            json.dump(rows, f)
+    print(json.dumps(out), flush=True)
+
+
 def run_set(args):
     """Times every GEMM of a set over rotating HBM-resident copies and reports
     TFLOP/s and the fraction of each shape's roofline."""
@@ -508,6 +575,9 @@ def main():
         vx.vx_calibration_enable(0)
     if args.study:
         run_study(args)
+        return
+    if args.adapt:
+        run_adapt(args)
         return
     if args.workload != "sweep":
         run_set(args)

@@ -213,6 +213,18 @@ vx_status vx_force_plan(int kernel_id, int split_k);
 vx_status vx_fix_wavefront(int wave_m, int wave_n, int mfma_m);
 
 /*
+ * Hardware-adaptation ablation (Section 7.4, "Dynamic Hardware Adaptation";
+ * the adaptive backend choice of Section 6.2): restrict every following
+ * selection to the matrix-core kernels (mask 1: families 0 and 1), to the
+ * vector-ALU kernels (mask 2: family 2), or lift the restriction (3, or 0).
+ * VX_ERR_INVALID_ARG for a mask outside 0..3, VX_ERR_NO_CANDIDATE if no
+ * enabled kernel is left; calls that no allowed kernel serves (dtype,
+ * alignment, K beyond a kernel's k_max) return VX_ERR_NO_CANDIDATE.
+ * Process-wide; for studies and tests.
+ */
+vx_status vx_restrict_backends(int mask);
+
+/*
  * Hand the library a caller-owned device buffer to use as the split-K
  * workspace of `stream` (NULL/0 bytes: return to the library's own lazily
  * allocated buffer).  The buffer must stay valid until the stream's work

@@ -35,6 +35,7 @@ vx_hwinfo g_hw[kMaxDevices];
 std::atomic<int> g_force_id{-1};
 std::atomic<int> g_force_split{0};
 std::atomic<int> g_fix_wm{0}, g_fix_wn{0}, g_fix_mi{0};
+std::atomic<int> g_backends{3};   // kernel backends the selector may use (vx_restrict_backends)
 std::atomic<uint64_t> g_epoch{0};   // bumps when planning inputs change
 
 struct PlanKey {
@@ -213,6 +214,7 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
     f.wave_m = g_fix_wm.load();
     f.wave_n = g_fix_wn.load();
     f.mfma_m = g_fix_mi.load();
+    f.backends = g_backends.load();
     vx_hwinfo hw;
     vx_status st = hwinfo_for(dev, &hw);
     if (st != VX_OK)
@@ -563,6 +565,26 @@ vx_status vx_force_plan(int kernel_id, int split_k)
         return VX_ERR_NO_CANDIDATE;
     g_force_id.store(kernel_id < 0 ? -1 : kernel_id);
     g_force_split.store(split_k > 0 ? split_k : 0);
+    return VX_OK;
+}
+
+vx_status vx_restrict_backends(int mask)
+{
+    if (mask < 0 || mask > 3)
+        return VX_ERR_INVALID_ARG;
+    if (mask == 0)
+        mask = 3;
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    bool any = false;
+    for (int i = 0; i < n && !any; ++i)
+        any = reg[i].info.enabled && (mask & (reg[i].info.family == 2 ? 2 : 1));
+    if (!any)
+        return VX_ERR_NO_CANDIDATE;
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_backends.store(mask);
+    g_plans.clear();
+    g_epoch.fetch_add(1);
     return VX_OK;
 }
 

@@ -210,6 +210,8 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
         const vx_kernel_info& k = reg[i].info;
         if ((forced_id >= 0 && k.id != forced_id) || !vxi_wave_matches(f, k))
             continue;
+        if (!(f.backends & (k.family == 2 ? 2 : 1)))
+            continue;
         for (int s : kSplits) {
             int split = s;
             if (forced_split > 0) {

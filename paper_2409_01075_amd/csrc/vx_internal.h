@@ -59,6 +59,7 @@ struct VxFilter {
     int kernel_id = -1;   // >= 0: only this kernel (a fixed workgroup and wavefront strategy)
     int split = 0;        // > 0: only this split-K factor
     int wave_m = 0, wave_n = 0, mfma_m = 0;   // > 0: only kernels with this wavefront strategy
+    int backends = 3;     // bit 0: matrix-core (MFMA) kernels, bit 1: vector-ALU kernels
 };
 
 // True if kernel k passes the wavefront part of the filter.

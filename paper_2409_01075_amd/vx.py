@@ -89,6 +89,8 @@ def lib():
     L.vx_force_plan.restype = i32
     L.vx_fix_wavefront.argtypes = [i32, i32, i32]
     L.vx_fix_wavefront.restype = i32
+    L.vx_restrict_backends.argtypes = [i32]
+    L.vx_restrict_backends.restype = i32
     L.vx_set_workspace.argtypes = [vp, ctypes.c_size_t, vp]
     L.vx_set_workspace.restype = i32
     L.vx_calibration_load.argtypes = [ctypes.c_char_p, ctypes.POINTER(i32)]
@@ -171,6 +173,13 @@ def vx_force_plan(kernel_id, split_k=0):
 
 def vx_fix_wavefront(wave_m=0, wave_n=0, mfma_m=0):
     return lib().vx_fix_wavefront(wave_m, wave_n, mfma_m)
+
+
+BACKEND_MFMA, BACKEND_VALU = 1, 2
+
+
+def vx_restrict_backends(mask=0):
+    return lib().vx_restrict_backends(mask)
 
 
 def vx_set_workspace(ptr, nbytes, stream=None):

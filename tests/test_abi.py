@@ -338,3 +338,24 @@ def test_one_hip_runtime_when_the_binding_loads_first():
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
     assert out.returncode == 0, out.stderr[-2000:]
     assert out.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_backend_restriction(mi355x_override):
+    """The hardware-adaptation hook: the argmin runs over the matrix-core
+    kernels only, the vector-ALU kernels only, or both."""
+    try:
+        assert vx.vx_restrict_backends(vx.BACKEND_VALU) == 0
+        p = vx.vx_plan_query(1, 3, 1024, 1024, vx.VX_BF16)
+        assert p.kernel.family == 2 and p.kernel.mfma_m == 0
+        assert vx.vx_restrict_backends(vx.BACKEND_MFMA) == 0
+        p = vx.vx_plan_query(1, 3, 1024, 1024, vx.VX_BF16)
+        assert p.kernel.family in (0, 1) and p.kernel.mfma_m > 0
+        assert vx.vx_restrict_backends(4) == 1 and vx.vx_restrict_backends(-1) == 1
+        # the vector-ALU kernels need 16-byte rows: element-aligned calls have no candidate
+        assert vx.vx_restrict_backends(vx.BACKEND_VALU) == 0
+        with pytest.raises(vx.VxError):
+            vx.vx_plan_query(1, 3, 1023, 1023, vx.VX_BF16)
+    finally:
+        assert vx.vx_restrict_backends(0) == 0
+    p = vx.vx_plan_query(1, 3, 1024, 1024, vx.VX_BF16)
+    assert p.kernel_id >= 0
