@@ -1,11 +1,12 @@
-"""CPU oracle for C = A x B — TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for C = A x B and the 2-D convolution — TEST INFRASTRUCTURE ONLY.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  The GEMM library never calls it, and it
 shares no code with the library: its own fp16/bf16 codec, its own loops.
 
 The arithmetic lives in ``oracle.c`` (plain C, binary64, k ascending; the
-definition of Section 4.1).  This module only marshals numpy arrays into it.
+definition of Section 4.1; the direct convolution of Section 7.1, Table 4).
+This module only marshals numpy arrays into it.
 
 Pins (tests/test_oracle_pins.py) tie it to facts outside itself: exact
 rational brute force on tiny shapes, numpy's float64 matmul, identity and
@@ -39,6 +40,10 @@ def _load():
     lib.oracle_gemm_sampled.argtypes = [ip, i64, i64, i64, vp, i64, vp, i64, i64,
                                         vp, vp, vp, dp, dp]
     lib.oracle_gemm_sampled.restype = ctypes.c_int
+    lib.oracle_conv2d.argtypes = [ip] + [i64] * 13 + [vp, vp, dp, dp, ip]
+    lib.oracle_conv2d.restype = ctypes.c_int
+    lib.oracle_conv_out_dim.argtypes = [i64] * 5
+    lib.oracle_conv_out_dim.restype = i64
     lib.oracle_encode.argtypes = [ip, dp, vp, i64]
     lib.oracle_encode.restype = None
     lib.oracle_decode.argtypes = [ip, vp, dp, i64]
@@ -157,3 +162,33 @@ def gemm_sampled(A, B, dtype, M, N, K, rows, cols, bats=None, sA=None, sB=None):
     if rc != 0:
         raise RuntimeError("oracle_gemm_sampled failed (rc=%d)" % rc)
     return ref, mag
+
+
+def conv_out_dim(size, k, stride, pad, dil):
+    """Output extent of a convolution along one axis (0 if nothing fits)."""
+    return int(_load().oracle_conv_out_dim(size, k, stride, pad, dil))
+
+
+def conv2d(x, w, dtype, stride=(1, 1), pad=(0, 0), dil=(1, 1), threads=None, with_mag=True):
+    """Reference 2-D convolution in float64 (plus Mag) for stored inputs.
+
+    x: N x H x W x Cin storage; w: KH x KW x Cin x Cout storage.  Returns
+    (out, Mag) shaped N x OH x OW x Cout (or out alone without Mag).
+    """
+    code = dtype_code(dtype)
+    xs = _as_storage(x, code)
+    ws = _as_storage(w, code)
+    if xs.ndim != 4 or ws.ndim != 4 or xs.shape[3] != ws.shape[2]:
+        raise ValueError("x must be N x H x W x Cin and w KH x KW x Cin x Cout")
+    N, H, W, Cin = xs.shape
+    KH, KW, _, Cout = ws.shape
+    OH = conv_out_dim(H, KH, stride[0], pad[0], dil[0])
+    OW = conv_out_dim(W, KW, stride[1], pad[1], dil[1])
+    out = np.zeros((N, OH, OW, Cout), dtype=np.float64)
+    mag = np.zeros((N, OH, OW, Cout), dtype=np.float64) if with_mag else None
+    rc = _load().oracle_conv2d(code, N, H, W, Cin, Cout, KH, KW, stride[0], stride[1], pad[0], pad[1],
+                               dil[0], dil[1], xs.ctypes.data, ws.ctypes.data, out.ctypes.data,
+                               mag.ctypes.data if with_mag else None, threads or default_threads())
+    if rc != 0:
+        raise RuntimeError("oracle_conv2d failed (rc=%d)" % rc)
+    return (out, mag) if with_mag else out

@@ -1,5 +1,6 @@
 /*
- * CPU oracle for the dense GEMM C = A x B (test infrastructure only).
+ * CPU oracle for the dense GEMM C = A x B and the 2-D convolution (test
+ * infrastructure only).
  *
  * Only the test suite, the smoke check and the CPU-baseline leg of the
  * benchmark may load this file's library.  The product path never calls it.
@@ -267,5 +268,122 @@ int oracle_gemm_sampled(int dtype, int64_t M, int64_t N, int64_t K,
         if (mag)
             mag[s] = m;
     }
+    return 0;
+}
+
+/* ---- the 2-D convolution ------------------------------------------------ */
+
+/*
+ * Direct 2-D convolution (the paper's second operator, Section 7.1,
+ * benchmarked in Table 4), as deep-learning layers compute it: a
+ * cross-correlation with zero padding, stride and dilation.
+ *
+ *   out[n][oh][ow][co] = sum_{kh, kw, ci} x[n][ih][iw][ci] * w[kh][kw][ci][co],
+ *   ih = oh*sh - ph + kh*dh,  iw = ow*sw - pw + kw*dw,
+ *
+ * where taps with (ih, iw) outside the H x W image are absent (zero padding),
+ * OH = floor((H + 2*ph - dh*(KH-1) - 1) / sh) + 1 (likewise OW; 0 when the
+ * numerator is negative).  Layouts: x is N x H x W x Cin, w is KH x KW x Cin
+ * x Cout, out is N x OH x OW x Cout, all dense.  Binary64, summation over kh,
+ * then kw, then ci ascending; Mag sums the absolute products.
+ */
+typedef struct {
+    const double *x, *w;
+    double *out, *mag;
+    int64_t H, W, Cin, Cout, KH, KW, sh, sw, ph, pw, dh, dw, OH, OW;
+    int64_t r0, r1;              /* output rows (n*OH + oh) handled by this thread */
+} conv_job;
+
+static void *conv_rows(void *arg)
+{
+    conv_job *j = (conv_job *)arg;
+    int64_t row, ow, kh, kw, ci, co;
+    for (row = j->r0; row < j->r1; ++row) {
+        int64_t n = row / j->OH, oh = row % j->OH;
+        for (ow = 0; ow < j->OW; ++ow) {
+            double *o = j->out + (row * j->OW + ow) * j->Cout;
+            double *m = j->mag ? j->mag + (row * j->OW + ow) * j->Cout : NULL;
+            for (co = 0; co < j->Cout; ++co) {
+                o[co] = 0.0;
+                if (m)
+                    m[co] = 0.0;
+            }
+            for (kh = 0; kh < j->KH; ++kh) {
+                int64_t ih = oh * j->sh - j->ph + kh * j->dh;
+                if (ih < 0 || ih >= j->H)
+                    continue;
+                for (kw = 0; kw < j->KW; ++kw) {
+                    int64_t iw = ow * j->sw - j->pw + kw * j->dw;
+                    if (iw < 0 || iw >= j->W)
+                        continue;
+                    const double *xp = j->x + ((n * j->H + ih) * j->W + iw) * j->Cin;
+                    for (ci = 0; ci < j->Cin; ++ci) {
+                        double a = xp[ci];
+                        const double *wp = j->w + ((kh * j->KW + kw) * j->Cin + ci) * j->Cout;
+                        for (co = 0; co < j->Cout; ++co)
+                            o[co] += a * wp[co];
+                        if (m) {
+                            double aa = fabs(a);
+                            for (co = 0; co < j->Cout; ++co)
+                                m[co] += aa * fabs(wp[co]);
+                        }
+                    }
+                }
+            }
+        }
+    }
+    return NULL;
+}
+
+int64_t oracle_conv_out_dim(int64_t in, int64_t k, int64_t stride, int64_t pad, int64_t dil)
+{
+    int64_t span = in + 2 * pad - dil * (k - 1) - 1;
+    return span < 0 ? 0 : span / stride + 1;
+}
+
+int oracle_conv2d(int dtype, int64_t N, int64_t H, int64_t W, int64_t Cin, int64_t Cout, int64_t KH,
+                  int64_t KW, int64_t sh, int64_t sw, int64_t ph, int64_t pw, int64_t dh, int64_t dw,
+                  const void *x, const void *w, double *out, double *mag, int threads)
+{
+    if (dtype < 0 || dtype > 2 || N < 0 || H < 0 || W < 0 || Cin < 0 || Cout < 0 || KH < 1 || KW < 1 ||
+        sh < 1 || sw < 1 || ph < 0 || pw < 0 || dh < 1 || dw < 1)
+        return -1;
+    int64_t OH = oracle_conv_out_dim(H, KH, sh, ph, dh), OW = oracle_conv_out_dim(W, KW, sw, pw, dw);
+    if (N == 0 || OH == 0 || OW == 0 || Cout == 0)
+        return 0;
+    if (threads < 1)
+        threads = 1;
+    int64_t nx = N * H * W * Cin, nw = KH * KW * Cin * Cout;
+    double *xd = (double *)malloc(sizeof(double) * (size_t)(nx > 0 ? nx : 1));
+    double *wd = (double *)malloc(sizeof(double) * (size_t)(nw > 0 ? nw : 1));
+    pthread_t *tid = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)threads);
+    conv_job *jobs = (conv_job *)malloc(sizeof(conv_job) * (size_t)threads);
+    if (!xd || !wd || !tid || !jobs) {
+        free(xd); free(wd); free(tid); free(jobs);
+        return -1;
+    }
+    oracle_decode(dtype, x, xd, nx);
+    oracle_decode(dtype, w, wd, nw);
+    int64_t rows = N * OH;
+    int t, nt = threads;
+    if (nt > rows)
+        nt = (int)rows;
+    for (t = 0; t < nt; ++t) {
+        conv_job *j = &jobs[t];
+        j->x = xd; j->w = wd; j->out = out; j->mag = mag;
+        j->H = H; j->W = W; j->Cin = Cin; j->Cout = Cout; j->KH = KH; j->KW = KW;
+        j->sh = sh; j->sw = sw; j->ph = ph; j->pw = pw; j->dh = dh; j->dw = dw; j->OH = OH; j->OW = OW;
+        j->r0 = rows * t / nt;
+        j->r1 = rows * (t + 1) / nt;
+    }
+    if (nt == 1) {
+        conv_rows(&jobs[0]);
+    } else {
+        for (t = 0; t < nt; ++t)
+            pthread_create(&tid[t], NULL, conv_rows, &jobs[t]);
+        for (t = 0; t < nt; ++t)
+            pthread_join(tid[t], NULL);
+    }
+    free(xd); free(wd); free(tid); free(jobs);
     return 0;
 }

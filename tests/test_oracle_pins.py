@@ -260,3 +260,138 @@ def test_exact_range_helper():
             r = I.exact_range(K, code)
             assert K * r * r <= 2 ** p
             assert K * (r + 1) * (r + 1) > 2 ** p
+
+
+# ------------------------------------------------------------ convolution ----
+# The direct convolution (N x H x W x Cin input, KH x KW x Cin x Cout filter,
+# zero padding, stride, dilation) pinned to outside facts.
+
+def _conv_cases(g, n):
+    for _ in range(n):
+        N, H, W = int(g.integers(1, 3)), int(g.integers(1, 6)), int(g.integers(1, 6))
+        Cin, Cout, KH, KW = int(g.integers(1, 4)), int(g.integers(1, 4)), int(g.integers(1, 4)), int(g.integers(1, 4))
+        st = (int(g.integers(1, 3)), int(g.integers(1, 3)))
+        pd = (int(g.integers(0, 3)), int(g.integers(0, 3)))
+        dl = (int(g.integers(1, 3)), int(g.integers(1, 3)))
+        yield N, H, W, Cin, Cout, KH, KW, st, pd, dl
+
+
+@pytest.mark.parametrize("code", [F32, F16, BF16])
+def test_conv_bruteforce_exact_rational(code):
+    """Every tap enumerated in exact rational arithmetic from the layer's
+    definition; the oracle is within its own binary64 rounding of it."""
+    g = I.rng(900 + code)
+    for (N, H, W, Cin, Cout, KH, KW, st, pd, dl) in _conv_cases(g, 40):
+        x = I.uniform(g, (N, H, W, Cin), code)
+        w = I.uniform(g, (KH, KW, Cin, Cout), code)
+        xd, wd = oracle.decode(x, code), oracle.decode(w, code)
+        ref, mag = oracle.conv2d(x, w, code, st, pd, dl)
+        OH, OW = ref.shape[1], ref.shape[2]
+        assert OH == max(0, (H + 2 * pd[0] - dl[0] * (KH - 1) - 1) // st[0] + 1)
+        assert OW == max(0, (W + 2 * pd[1] - dl[1] * (KW - 1) - 1) // st[1] + 1)
+        K = KH * KW * Cin
+        for n in range(N):
+            for oh in range(OH):
+                for ow in range(OW):
+                    for co in range(Cout):
+                        exact = Fraction(0)
+                        for kh in range(KH):
+                            for kw in range(KW):
+                                ih = oh * st[0] - pd[0] + kh * dl[0]
+                                iw = ow * st[1] - pd[1] + kw * dl[1]
+                                if 0 <= ih < H and 0 <= iw < W:
+                                    for ci in range(Cin):
+                                        exact += Fraction(xd[n, ih, iw, ci]) * Fraction(wd[kh, kw, ci, co])
+                        err = abs(Fraction(ref[n, oh, ow, co]) - exact)
+                        assert err <= Fraction(K) * Fraction(2) ** -53 * Fraction(mag[n, oh, ow, co])
+
+
+def test_conv_matches_torch_float64():
+    """PyTorch's CPU convolution in binary64 (NCHW, so the test permutes)."""
+    torch = pytest.importorskip("torch")
+    g = I.rng(910)
+    for (N, H, W, Cin, Cout, KH, KW, st, pd, dl) in list(_conv_cases(g, 25)) + [(2, 17, 13, 5, 7, 3, 3, (2, 1), (1, 2), (1, 1))]:
+        x = I.uniform(g, (N, H, W, Cin), F32)
+        w = I.uniform(g, (KH, KW, Cin, Cout), F32)
+        ref, mag = oracle.conv2d(x, w, F32, st, pd, dl)
+        if ref.size == 0:
+            continue
+        xt = torch.from_numpy(x.astype(np.float64)).permute(0, 3, 1, 2)
+        wt = torch.from_numpy(w.astype(np.float64)).permute(3, 2, 0, 1)
+        want = torch.nn.functional.conv2d(xt, wt, stride=st, padding=pd, dilation=dl).permute(0, 2, 3, 1).numpy()
+        assert want.shape == ref.shape
+        assert np.all(np.abs(ref - want) <= 1e-12 * mag + 1e-300)
+
+
+def test_conv_1x1_is_matmul():
+    """A 1 x 1, stride-1, unpadded convolution is the GEMM of the pixels by the filter."""
+    g = I.rng(920)
+    x = I.uniform(g, (3, 7, 5, 11), F32)
+    w = I.uniform(g, (1, 1, 11, 6), F32)
+    ref, mag = oracle.conv2d(x, w, F32)
+    want = x.astype(np.float64).reshape(-1, 11) @ w.astype(np.float64).reshape(11, 6)
+    assert np.all(np.abs(ref.reshape(-1, 6) - want) <= 1e-12 * mag.reshape(-1, 6))
+
+
+def test_conv_matches_scipy_correlate2d():
+    """Single channel, stride 1: scipy's 2-D cross-correlation (zero-padded input)."""
+    signal = pytest.importorskip("scipy.signal")
+    g = I.rng(930)
+    for (H, W, KH, KW, ph, pw) in ((6, 5, 3, 2, 0, 0), (4, 7, 2, 3, 1, 2), (5, 5, 5, 5, 2, 2), (3, 8, 1, 4, 0, 3)):
+        x = I.uniform(g, (1, H, W, 1), F32)
+        w = I.uniform(g, (KH, KW, 1, 1), F32)
+        ref = oracle.conv2d(x, w, F32, (1, 1), (ph, pw), (1, 1), with_mag=False)
+        xp = np.pad(x[0, :, :, 0].astype(np.float64), ((ph, ph), (pw, pw)))
+        want = signal.correlate2d(xp, w[:, :, 0, 0].astype(np.float64), mode="valid")
+        assert np.allclose(ref[0, :, :, 0], want, rtol=0, atol=1e-12)
+
+
+def test_conv_delta_filter_moves_the_input():
+    """A filter that is the identity channel map at one tap (kh0, kw0) copies
+    the input pixel that tap reads: exact, zeros where it falls in the padding."""
+    g = I.rng(940)
+    for code in (F32, F16, BF16):
+        N, H, W, C, KH, KW = 2, 7, 6, 3, 3, 2
+        st, pd, dl = (2, 1), (2, 1), (1, 2)
+        x = I.uniform(g, (N, H, W, C), code)
+        for kh0 in range(KH):
+            for kw0 in range(KW):
+                wd = np.zeros((KH, KW, C, C))
+                wd[kh0, kw0] = np.eye(C)
+                ref = oracle.conv2d(x, oracle.encode(wd, code), code, st, pd, dl, with_mag=False)
+                xd = oracle.decode(x, code)
+                for oh in range(ref.shape[1]):
+                    for ow in range(ref.shape[2]):
+                        ih, iw = oh * st[0] - pd[0] + kh0 * dl[0], ow * st[1] - pd[1] + kw0 * dl[1]
+                        want = xd[:, ih, iw, :] if (0 <= ih < H and 0 <= iw < W) else 0.0
+                        assert np.array_equal(ref[:, oh, ow, :], np.broadcast_to(want, ref[:, oh, ow, :].shape))
+
+
+def test_conv_ones_count_the_taps_inside_the_image():
+    """All-ones input and filter: every output is Cin times the number of taps
+    whose (ih, iw) falls inside the image -- counted here independently."""
+    for (H, W, KH, KW, st, pd, dl) in ((5, 4, 3, 3, (1, 1), (1, 1), (1, 1)), (9, 7, 3, 2, (2, 3), (2, 1), (2, 1)),
+                                       (4, 4, 5, 5, (1, 1), (2, 2), (1, 1))):
+        C = 3
+        x = np.ones((1, H, W, C), dtype=np.float32)
+        w = np.ones((KH, KW, C, 2), dtype=np.float32)
+        ref = oracle.conv2d(x, w, F32, st, pd, dl, with_mag=False)
+        for oh in range(ref.shape[1]):
+            rows = sum(1 for kh in range(KH) if 0 <= oh * st[0] - pd[0] + kh * dl[0] < H)
+            for ow in range(ref.shape[2]):
+                cols = sum(1 for kw in range(KW) if 0 <= ow * st[1] - pd[1] + kw * dl[1] < W)
+                assert np.all(ref[0, oh, ow] == C * rows * cols)
+
+
+def test_conv_stride_subsamples_and_dilation_spreads_the_filter():
+    g = I.rng(950)
+    x = I.uniform(g, (2, 11, 10, 3), F32)
+    w = I.uniform(g, (3, 3, 3, 4), F32)
+    full = oracle.conv2d(x, w, F32, (1, 1), (1, 1), (1, 1), with_mag=False)
+    strided = oracle.conv2d(x, w, F32, (2, 3), (1, 1), (1, 1), with_mag=False)
+    assert np.array_equal(strided, full[:, ::2, ::3, :])
+    # dilation 2 == the filter with a zero between taps, undilated
+    wd = np.zeros((5, 5, 3, 4), dtype=np.float32)
+    wd[::2, ::2] = w
+    assert np.array_equal(oracle.conv2d(x, w, F32, (1, 1), (2, 2), (2, 2), with_mag=False),
+                          oracle.conv2d(x, wd, F32, (1, 1), (2, 2), (1, 1), with_mag=False))
