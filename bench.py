@@ -265,7 +265,7 @@ def run_study(args):
     e1.record(stream)
     torch.cuda.synchronize()
     spin = int(1e6 / max(e0.elapsed_time(e1), 1e-3) * 0.3)
-    reg = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]
+    reg = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count())) if k.op == 0]
     jobs = _set_jobs(args.workload, args.trials)
     rows, tables = [], []
     vx.vx_force_plan(-1, 0)

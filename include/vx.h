@@ -98,6 +98,8 @@ typedef struct vx_kernel_info {
     int enabled;
     int k_max;                     /* longest K slice one workgroup takes (0: unbounded); family 2
                                       keeps its slice of A in LDS */
+    int op;                        /* 0: GEMM; 1: 2-D convolution (implicit GEMM: A is the input
+                                      image read through the im2col map) */
 } vx_kernel_info;
 
 /* A concrete execution plan for one call. */
@@ -233,6 +235,36 @@ vx_status vx_restrict_backends(int mask);
  * 256 KiB + the partials of the plans that will run.
  */
 vx_status vx_set_workspace(void* ptr, size_t bytes, void* stream);
+
+/*
+ * 2-D convolution (the paper's second operator, Section 7.1 and Table 4) on
+ * the same hierarchy, as an implicit GEMM: M = n*oh*ow output pixels,
+ * N = c_out, K = kh*kw*c_in, the A tile gathered from the image through the
+ * im2col map, the filter read as a K x c_out row-major matrix.
+ *
+ *   y[n][oh][ow][co] = sum_{kh, kw, ci} x[n][ih][iw][ci] * w[kh][kw][ci][co],
+ *   ih = oh*stride_h - pad_h + kh*dil_h,  iw = ow*stride_w - pad_w + kw*dil_w,
+ *
+ * with taps outside the h x w image absent (zero padding) and
+ * oh = (h + 2*pad_h - dil_h*(kh-1) - 1) / stride_h + 1 (likewise ow; no output
+ * when the numerator is negative).  Layouts (dense, element-aligned pointers
+ * allowed): x n x h x w x c_in, w kh x kw x c_in x c_out, y n x oh x ow x
+ * c_out.  fp32 accumulation; y rounded to nearest even in `dtype`.
+ * Ownership and errors as for vx_gemm: sizes < 0, kh/kw/strides/dilations
+ * < 1, pads < 0, extents beyond 32-bit element counts, a NULL operand with a
+ * non-empty extent, or y overlapping x or w -> VX_ERR_INVALID_ARG; an empty
+ * output is a no-op; c_in = 0 writes zeros.  Asynchronous on `stream`.
+ */
+typedef struct vx_conv2d_desc {
+    int64_t n, h, w, c_in, c_out, kh, kw;
+    int64_t stride_h, stride_w, pad_h, pad_w, dil_h, dil_w;
+    vx_dtype dtype;
+} vx_conv2d_desc;
+
+vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void* y, void* stream);
+
+/* The plan vx_conv2d would run for `d` (host only, no launch). */
+vx_status vx_conv2d_plan_query(const vx_conv2d_desc* d, vx_plan* out);
 
 const char* vx_status_string(vx_status s);
 const char* vx_version(void);

@@ -102,10 +102,16 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
             a0, b0, cc = (X.data_ptr() + sh * eb for X in (A, B, C))
             sa, sb, sc = M * K * eb, K * N * eb, M * N * eb
             vx.vx_force_plan(kid, split)
+            # a convolution kernel runs the same implicit-GEMM shape as a 1 x 1
+            # convolution of a 1 x M image with K channels into N
+            desc = vx.conv_desc(1, 1, M, K, N, 1, 1, k.dtype) if k.op == 1 else None
             try:
                 def call(i):
                     r = i % R
-                    st = L.vx_gemm(M, N, K, k.dtype, a0 + r * sa, b0 + r * sb, cc + r * sc, sp)
+                    if desc is not None:
+                        st = vx.vx_conv2d(desc, a0 + r * sa, b0 + r * sb, cc + r * sc, sp)
+                    else:
+                        st = L.vx_gemm(M, N, K, k.dtype, a0 + r * sa, b0 + r * sb, cc + r * sc, sp)
                     if st != 0:
                         raise RuntimeError("kernel %d: %s" % (kid, vx.STATUS.get(st, st)))
                 call(0)

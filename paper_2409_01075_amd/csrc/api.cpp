@@ -43,10 +43,11 @@ struct PlanKey {
     int dt, vec_ok, c_vec, dev;
     size_t ws;
     uint64_t epoch;
+    int op;
     bool operator==(const PlanKey& o) const
     {
         return batch == o.batch && M == o.M && N == o.N && K == o.K && dt == o.dt && vec_ok == o.vec_ok &&
-               c_vec == o.c_vec && dev == o.dev && ws == o.ws && epoch == o.epoch;
+               c_vec == o.c_vec && dev == o.dev && ws == o.ws && epoch == o.epoch && op == o.op;
     }
 };
 struct PlanKeyHash {
@@ -55,7 +56,7 @@ struct PlanKeyHash {
         uint64_t h = 1469598103934665603ull;
         auto mix = [&h](uint64_t v) { h = (h ^ v) * 1099511628211ull; };
         mix(k.batch); mix(k.M); mix(k.N); mix(k.K);
-        mix(k.dt | (k.vec_ok << 4) | (k.c_vec << 5) | ((uint64_t)k.dev << 8));
+        mix(k.dt | (k.vec_ok << 4) | (k.c_vec << 5) | (k.op << 6) | ((uint64_t)k.dev << 8));
         mix(k.ws); mix(k.epoch);
         return (size_t)h;
     }
@@ -225,7 +226,7 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
     lim.max_tickets = ws_bytes ? (int64_t)(kTicketBytes / 4) : 0;
     if (f.kernel_id >= 0)
         return vxi_select(hw, sh, lim, f, out);
-    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, epoch};
+    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, epoch, sh.op};
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_plans.find(key);
@@ -279,6 +280,8 @@ vx_status ws_get(int dev, void* stream, Workspace* out)
     return VX_OK;
 }
 
+vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream);
+
 vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
                     int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, void* stream)
 {
@@ -311,6 +314,21 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
                 strides_vec;
     sh.c_vec = (N % 4 == 0) && ((uintptr_t)C % (4 * eb) == 0) && (batch == 1 || sC % 4 == 0);
 
+    VxGemmArgs a = {};
+    a.A = A;
+    a.B = B;
+    a.C = C;
+    a.sA = sA;
+    a.sB = sB;
+    a.sC = sC;
+    return plan_and_launch(sh, a, stream);
+}
+
+// Plans shape `sh` on the current device and launches the chosen kernel with
+// the operand fields of `a` (pointers, batch strides, convolution shape);
+// the size and grid fields are filled in here.
+vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream)
+{
     int dev = 0;
     vx_status st = current_device(&dev);
     if (st != VX_OK)
@@ -341,21 +359,14 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
     if (st != VX_OK)
         return st;
 
-    VxGemmArgs a;
-    a.A = A;
-    a.B = B;
-    a.C = C;
-    a.sA = sA;
-    a.sB = sB;
-    a.sC = sC;
-    a.M = (int)M;
-    a.N = (int)N;
-    a.K = (int)K;
+    a.M = (int)sh.M;
+    a.N = (int)sh.N;
+    a.K = (int)sh.K;
     a.tiles_m = (int)plan.tiles_m;
     a.tiles_n = (int)plan.tiles_n;
     a.split = plan.split_k;
     a.k_per_split = plan.k_per_split;
-    a.batch = (int)batch;
+    a.batch = (int)sh.batch;
     a.group_m = plan.group_m;
     a.num_xcd = hw.num_xcd;
     a.grid = (int)plan.grid;
@@ -366,6 +377,59 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
         (void)hipGetLastError();
         return VX_ERR_HIP;
     }
+    return VX_OK;
+}
+
+int64_t conv_out_dim(int64_t in, int64_t k, int64_t stride, int64_t pad, int64_t dil)
+{
+    const int64_t span = in + 2 * pad - dil * (k - 1) - 1;
+    return span < 0 ? 0 : span / stride + 1;
+}
+
+// Checks a convolution descriptor and maps it to its implicit-GEMM shape;
+// fills the convolution fields of `a`.  Sets *empty for an empty output.
+vx_status conv_shape(const vx_conv2d_desc* d, VxShape* sh, VxGemmArgs* a, bool* empty)
+{
+    if (!d)
+        return VX_ERR_INVALID_ARG;
+    if (d->dtype != VX_F32 && d->dtype != VX_F16 && d->dtype != VX_BF16)
+        return VX_ERR_UNSUPPORTED_DTYPE;
+    if (d->n < 0 || d->h < 0 || d->w < 0 || d->c_in < 0 || d->c_out < 0 || d->kh < 1 || d->kw < 1 ||
+        d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0 || d->dil_h < 1 || d->dil_w < 1)
+        return VX_ERR_INVALID_ARG;
+    const int64_t lim = INT32_MAX;
+    if (d->h > lim || d->w > lim || d->kh > lim || d->kw > lim || d->pad_h > lim / 4 || d->pad_w > lim / 4 ||
+        d->stride_h > lim || d->stride_w > lim || d->dil_h > lim || d->dil_w > lim)
+        return VX_ERR_INVALID_ARG;
+    const int64_t oh = conv_out_dim(d->h, d->kh, d->stride_h, d->pad_h, d->dil_h);
+    const int64_t ow = conv_out_dim(d->w, d->kw, d->stride_w, d->pad_w, d->dil_w);
+    // every element index the kernels form stays within 32 bits, except the
+    // image offset, which they form in 64 bits
+    const double M = (double)d->n * oh * ow, K = (double)d->kh * d->kw * d->c_in;
+    if (M > lim || K > lim || d->c_out > lim || M * d->c_out > lim || K * d->c_out > lim ||
+        (double)d->n * d->h * d->w * d->c_in > 9.0e15)
+        return VX_ERR_INVALID_ARG;
+    *empty = M == 0 || d->c_out == 0;
+    sh->batch = 1;
+    sh->M = (int64_t)M;
+    sh->N = d->c_out;
+    sh->K = (int64_t)K;
+    sh->dt = d->dtype;
+    sh->vec_ok = 0;   // the conv kernels take element-aligned operands
+    sh->c_vec = 0;
+    sh->op = 1;
+    a->cH = (int)d->h;
+    a->cW = (int)d->w;
+    a->cC = (int)d->c_in;
+    a->cKW = (int)d->kw;
+    a->cOH = (int)oh;
+    a->cOW = (int)ow;
+    a->csh = (int)d->stride_h;
+    a->csw = (int)d->stride_w;
+    a->cph = (int)d->pad_h;
+    a->cpw = (int)d->pad_w;
+    a->cdh = (int)d->dil_h;
+    a->cdw = (int)d->dil_w;
     return VX_OK;
 }
 
@@ -482,6 +546,46 @@ vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype
     sh.c_vec = (N % 4 == 0) && (base_align % (4 * eb) == 0) && (batch == 1 || strideC % 4 == 0);
     int dev = 0;
     vx_status st = current_device(&dev);
+    if (st != VX_OK)
+        return st;
+    return plan_for(dev, sh, dev < 0 ? kDefaultPartials : ws_capacity(dev, nullptr), out);
+}
+
+vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void* y, void* stream)
+{
+    VxShape sh;
+    VxGemmArgs a = {};
+    bool empty = false;
+    vx_status st = conv_shape(d, &sh, &a, &empty);
+    if (st != VX_OK)
+        return st;
+    const int eb = elem_bytes(d->dtype);
+    const size_t ex = (size_t)(d->n * d->h * d->w * d->c_in), ew = (size_t)(d->kh * d->kw * d->c_in * d->c_out);
+    const size_t ey = (size_t)(sh.M * sh.N);
+    if ((ex && !empty && sh.K && !x) || (ew && !empty && !w) || (ey && !y))
+        return VX_ERR_INVALID_ARG;
+    if (overlaps(y, ey * eb, x, ex * eb) || overlaps(y, ey * eb, w, ew * eb))
+        return VX_ERR_INVALID_ARG;
+    if (empty)
+        return VX_OK;
+    a.A = x;
+    a.B = w;
+    a.C = y;
+    return plan_and_launch(sh, a, stream);
+}
+
+vx_status vx_conv2d_plan_query(const vx_conv2d_desc* d, vx_plan* out)
+{
+    VxShape sh;
+    VxGemmArgs a = {};
+    bool empty = false;
+    vx_status st = conv_shape(d, &sh, &a, &empty);
+    if (st != VX_OK)
+        return st;
+    if (!out || empty)
+        return VX_ERR_INVALID_ARG;
+    int dev = 0;
+    st = current_device(&dev);
     if (st != VX_OK)
         return st;
     return plan_for(dev, sh, dev < 0 ? kDefaultPartials : ws_capacity(dev, nullptr), out);

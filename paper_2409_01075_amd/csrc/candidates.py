@@ -235,7 +235,30 @@ def _entry(dtype, family, stages, c, vec, hw):
     mb, nb, kb, wm, wn, mi = c
     lds = lds_bytes_dma(mb, nb, kb, stages) if family == "dma" else lds_bytes(dtype, mb, nb, kb)
     return dict(dtype=dtype, dt=DT_CODE[dtype], family=family, stages=stages, mb=mb, nb=nb, kb=kb, wm=wm,
-                wn=wn, mi=mi, vec=vec, threads=wm * wn * hw["wave"], lds=lds, k_max=0)
+                wn=wn, mi=mi, vec=vec, threads=wm * wn * hw["wave"], lds=lds, k_max=0, op=0)
+
+
+# ------------------------------------------------ convolution (implicit GEMM) --
+# The paper's second operator on the same hierarchy: a convolution is the
+# GEMM of its output pixels (M = n*oh*ow) by its filter (K = kh*kw*c_in rows,
+# N = c_out columns), with the A tile gathered from the image through the
+# im2col map.  The conv kernels are register-staged, element-aligned
+# workgroup tiles of the GEMM candidates (the gather goes through VGPRs
+# anyway): one K step of 64 (16-bit) or 32 (fp32) elements, tiles from 32 x 32
+# to 128 x 128.
+CONV_TILES = {(32, 32), (32, 64), (64, 32), (64, 64), (64, 128), (128, 64), (128, 128)}
+
+
+def conv_candidates(dtype, hw=GFX950):
+    kb = 64 if ELEM_BYTES[dtype] == 2 else 32
+    out = []
+    for c in generate_candidates_for_layer(2, dtype, hw, "reg")[0]:
+        mb, nb, ckb, wm, wn, mi = c
+        if ckb == kb and (mb, nb) in CONV_TILES and wm * wn == 4:
+            e = _entry(dtype, "reg", 2, c, 0, hw)
+            e["op"] = 1
+            out.append(e)
+    return out
 
 
 # ------------------------------------------------- vector-ALU family (L0') --
@@ -269,7 +292,7 @@ def valu_candidates(dtype, hw=GFX950):
                 if regs > (512 if waves <= 4 else 256) or kmax < kpi or lds > hw["lds_bytes"] - LDS_RESERVE:
                     continue
                 out.append(dict(dtype=dtype, dt=DT_CODE[dtype], family="valu", stages=u, mb=mt, nb=nb, kb=kpi, wm=1,
-                                wn=waves, mi=0, vec=1, threads=waves * hw["wave"], lds=lds, k_max=kmax))
+                                wn=waves, mi=0, vec=1, threads=waves * hw["wave"], lds=lds, k_max=kmax, op=0))
     return out
 
 
@@ -298,6 +321,8 @@ def registry(hw=GFX950):
             out.append(_entry("f32", "reg", 2, c, vec, hw))
     for dtype in ("f16", "bf16", "f32"):
         out += valu_candidates(dtype, hw)
+    for dtype in ("f16", "bf16", "f32"):
+        out += conv_candidates(dtype, hw)
     for i, e in enumerate(out):
         e["id"] = i
     return out

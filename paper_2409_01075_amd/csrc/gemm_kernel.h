@@ -48,11 +48,13 @@ enum { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
 
 // Compile-time description of one candidate: workgroup tile Mb x Nb x Kb,
 // WM x WN wavefronts, MFMA instruction tile MI x MI, operands whose rows are
-// 16-byte aligned (VEC) or only element aligned.
-template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, bool VEC_>
+// 16-byte aligned (VEC) or only element aligned, and whether A is a plain
+// matrix or a convolution's input image (CONV: the implicit GEMM).
+template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, bool VEC_, bool CONV_ = false>
 struct Cfg {
     static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_;
     static constexpr bool VEC = VEC_;
+    static constexpr bool CONV = CONV_;                  // A is an image read through the im2col map
     static constexpr bool H = DT != DT_F32;              // 16-bit inputs
     static constexpr int NT = WM * WN * 64;              // threads per workgroup
     static constexpr int MW = MB / WM, NW = NB / WN;     // wavefront tile
@@ -119,9 +121,9 @@ struct Tile {
     __device__ __forceinline__ void load(const char* __restrict__ Ab, const char* __restrict__ Bb,
                                          int m0, int n0, int k0, int kend, int M, int N, int K, int t)
     {
-        // A: MB x KB, chunks along k
+        // A: MB x KB, chunks along k (a convolution gathers A in load_a_conv)
 #pragma unroll
-        for (int v = 0; v < C::AV; ++v) {
+        for (int v = 0; v < (C::CONV ? 0 : C::AV); ++v) {
             const int idx = t + v * C::NT;
             const int r = idx / (C::KB / C::VE), c = idx % (C::KB / C::VE);
             const int gm = m0 + r, gk = k0 + c * C::VE;
@@ -185,6 +187,63 @@ struct Tile {
                     rb[v] = x;
                 }
             }
+        }
+    }
+
+    // Convolution: the A tile's chunks gathered from the image through the
+    // im2col map.  Row gm of the implicit A is output pixel (n, oh, ow);
+    // column gk is filter tap (kh, kw) and input channel ci, with
+    // gk = (kh * KW + kw) * Cin + ci.  When Cin is a multiple of the chunk,
+    // a chunk never straddles two taps and is one 16-byte load (or zeros in
+    // the padding); otherwise it is gathered element by element.
+    __device__ __forceinline__ void load_a_conv(const VxGemmArgs& p, const char* __restrict__ X, int m0, int k0,
+                                                int kend, int t)
+    {
+        const bool whole = p.cC % C::VE == 0;   // wave-uniform
+#pragma unroll
+        for (int v = 0; v < C::AV; ++v) {
+            const int idx = t + v * C::NT;
+            const int r = idx / (C::KB / C::VE), c = idx % (C::KB / C::VE);
+            const int gm = m0 + r, gk = k0 + c * C::VE;
+            u32x4 x = {0, 0, 0, 0};
+            if (gm < p.M && gk < kend) {
+                const int ow = gm % p.cOW, q = gm / p.cOW;
+                const int oh = q % p.cOH, n = q / p.cOH;
+                const int ih0 = oh * p.csh - p.cph, iw0 = ow * p.csw - p.cpw;
+                if (whole) {
+                    const int ci = gk % p.cC, khw = gk / p.cC;
+                    const int ih = ih0 + (khw / p.cKW) * p.cdh, iw = iw0 + (khw % p.cKW) * p.cdw;
+                    if (ih >= 0 && ih < p.cH && iw >= 0 && iw < p.cW)
+                        x = *(const u32x4_u*)(X + (((int64_t)n * p.cH + ih) * p.cW + iw) * (int64_t)p.cC * C::EB +
+                                              (int64_t)ci * C::EB);
+                } else {
+                    unsigned e16[C::VE];
+#pragma unroll
+                    for (int e = 0; e < C::VE; ++e) {
+                        const int k = gk + e;
+                        unsigned val = 0u;
+                        if (k < kend) {
+                            const int ci = k % p.cC, khw = k / p.cC;
+                            const int ih = ih0 + (khw / p.cKW) * p.cdh, iw = iw0 + (khw % p.cKW) * p.cdw;
+                            if (ih >= 0 && ih < p.cH && iw >= 0 && iw < p.cW) {
+                                const char* src = X + ((((int64_t)n * p.cH + ih) * p.cW + iw) * p.cC + ci) * C::EB;
+                                val = C::H ? (unsigned)*(const uint16_t*)src : *(const unsigned*)src;
+                            }
+                        }
+                        e16[e] = val;
+                    }
+                    if (C::H) {
+#pragma unroll
+                        for (int e = 0; e < 8; e += 2)
+                            x[e >> 1] = pack2(e16[e], e16[e + 1]);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            x[e] = e16[e];
+                    }
+                }
+            }
+            ra[v] = x;
         }
     }
 
@@ -405,6 +464,13 @@ __device__ __forceinline__ VxGemmArgs pin_args(const VxGemmArgs& in)
                       "+s"(p.K), "+s"(p.tiles_m), "+s"(p.tiles_n), "+s"(p.split), "+s"(p.k_per_split),
                       "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.ws), "+s"(p.tickets));
     return p;
+}
+
+// The convolution's shape arguments, pinned like the others (conv kernels).
+__device__ __forceinline__ void pin_conv(VxGemmArgs& p)
+{
+    asm volatile("" : "+s"(p.cH), "+s"(p.cW), "+s"(p.cC), "+s"(p.cKW), "+s"(p.cOH), "+s"(p.cOW), "+s"(p.csh),
+                      "+s"(p.csw), "+s"(p.cph), "+s"(p.cpw), "+s"(p.cdh), "+s"(p.cdw));
 }
 
 // ---------------------------------------------------------- level 2 -------
@@ -671,7 +737,9 @@ __device__ __forceinline__ void store_lds(const VxGemmArgs& p, Acc<C>& acc, cons
 template <class C>
 __device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
 {
-    const VxGemmArgs p = pin_args(args);
+    VxGemmArgs p = pin_args(args);
+    if constexpr (C::CONV)
+        pin_conv(p);
     __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
 
     const int t = threadIdx.x;
@@ -687,15 +755,21 @@ __device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
     acc_zero<C>(acc);
 
     Tile<C> tl;
+    // one K step of A and B into registers (for a convolution, A through the im2col map)
+    auto load = [&](int k0) {
+        tl.load(Ab, Bb, 0, g.n0, k0, g.kend, Mrel, p.N, p.K, t);
+        if constexpr (C::CONV)
+            tl.load_a_conv(p, (const char*)p.A, g.m0, k0, g.kend, t);
+    };
     if (g.nk > 0) {
-        tl.load(Ab, Bb, 0, g.n0, g.kbeg, g.kend, Mrel, p.N, p.K, t);
+        load(g.kbeg);
         tl.store(smem, t);
     }
     __syncthreads();
     for (int it = 0; it < g.nk; ++it) {
         char* cur = smem + (it & 1) * C::STAGE_BYTES;
         if (it + 1 < g.nk)
-            tl.load(Ab, Bb, 0, g.n0, g.kbeg + (it + 1) * C::KB, g.kend, Mrel, p.N, p.K, t);
+            load(g.kbeg + (it + 1) * C::KB);
         compute_step<C>(cur, acc, wm0, wn0, lane);
         if (it + 1 < g.nk)
             tl.store(smem + ((it + 1) & 1) * C::STAGE_BYTES, t);

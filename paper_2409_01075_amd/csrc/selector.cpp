@@ -74,7 +74,7 @@ int vxi_occupancy(const vx_hwinfo& hw, const vx_kernel_info& k)
 double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k, int split,
                 const VxLimits& lim, int* k_per_split)
 {
-    if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || split < 1)
+    if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || split < 1 || k.op != sh.op)
         return -1.0;
     const int eb = sh.dt == VX_F32 ? 4 : 2;
     const int64_t tiles_m = cdiv(sh.M, k.mb), tiles_n = cdiv(sh.N, k.nb);

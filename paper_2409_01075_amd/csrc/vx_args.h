@@ -17,4 +17,9 @@ struct VxGemmArgs {
     int grid;               // workgroups in the launch: tiles_m * tiles_n * split * batch
     float* ws;              // split-K partial tiles (split > 1), fp32
     unsigned* tickets;      // one self-resetting arrival counter per output tile
+    // 2-D convolution as an implicit GEMM (conv kernels only): A is the input
+    // image x (N x H x W x Cin) read through the im2col map, M = N*OH*OW,
+    // K = KH*KW*Cin, B is the filter (KH*KW*Cin x Cout), C the output.
+    int cH, cW, cC, cKW, cOH, cOW;
+    int csh, csw, cph, cpw, cdh, cdw;   // stride, padding, dilation (height, width)
 };

@@ -39,6 +39,7 @@ struct VxShape {
     int dt;        // vx_dtype
     int vec_ok;    // operands allow 16-byte vector loads
     int c_vec;     // C allows 4-element vector stores
+    int op = 0;    // 0: GEMM; 1: 2-D convolution as an implicit GEMM (conv kernels only)
 };
 
 struct VxLimits {

@@ -30,7 +30,12 @@ class vx_kernel_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in (
         "id", "dtype", "mb", "nb", "kb", "wm", "wn", "mfma_m", "mfma_n", "mfma_k", "vec", "family", "stages",
         "threads",
-        "lds_bytes", "vgprs", "agprs", "sgprs", "scratch_bytes", "enabled", "k_max")]
+        "lds_bytes", "vgprs", "agprs", "sgprs", "scratch_bytes", "enabled", "k_max", "op")]
+
+
+class vx_conv2d_desc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("n", "h", "w", "c_in", "c_out", "kh", "kw", "stride_h", "stride_w",
+                                              "pad_h", "pad_w", "dil_h", "dil_w")] + [("dtype", ctypes.c_int)]
 
 
 class vx_plan(ctypes.Structure):
@@ -91,6 +96,10 @@ def lib():
     L.vx_fix_wavefront.restype = i32
     L.vx_restrict_backends.argtypes = [i32]
     L.vx_restrict_backends.restype = i32
+    L.vx_conv2d.argtypes = [ctypes.POINTER(vx_conv2d_desc), vp, vp, vp, vp]
+    L.vx_conv2d.restype = i32
+    L.vx_conv2d_plan_query.argtypes = [ctypes.POINTER(vx_conv2d_desc), ctypes.POINTER(vx_plan)]
+    L.vx_conv2d_plan_query.restype = i32
     L.vx_set_workspace.argtypes = [vp, ctypes.c_size_t, vp]
     L.vx_set_workspace.restype = i32
     L.vx_calibration_load.argtypes = [ctypes.c_char_p, ctypes.POINTER(i32)]
@@ -173,6 +182,21 @@ def vx_force_plan(kernel_id, split_k=0):
 
 def vx_fix_wavefront(wave_m=0, wave_n=0, mfma_m=0):
     return lib().vx_fix_wavefront(wave_m, wave_n, mfma_m)
+
+
+def conv_desc(n, h, w, c_in, c_out, kh, kw, dtype, stride=(1, 1), pad=(0, 0), dil=(1, 1)):
+    return vx_conv2d_desc(n, h, w, c_in, c_out, kh, kw, stride[0], stride[1], pad[0], pad[1], dil[0], dil[1],
+                          dtype)
+
+
+def vx_conv2d(desc, x, w, y, stream=None):
+    return lib().vx_conv2d(ctypes.byref(desc), x, w, y, stream)
+
+
+def vx_conv2d_plan_query(desc):
+    p = vx_plan()
+    _chk(lib().vx_conv2d_plan_query(ctypes.byref(desc), ctypes.byref(p)), "vx_conv2d_plan_query")
+    return p
 
 
 BACKEND_MFMA, BACKEND_VALU = 1, 2
@@ -274,3 +298,24 @@ def bmm(A, B, out=None, stream=None):
     _chk(vx_gemm_batched(bt, M, N, K, _torch_dtype_code(A), A.data_ptr(), M * K, B.data_ptr(), sB,
                          C.data_ptr(), M * N, _stream_ptr(stream)), "vx_gemm_batched")
     return C
+
+
+def conv2d(x, w, stride=(1, 1), padding=(0, 0), dilation=(1, 1), out=None, stream=None):
+    """y = conv2d(x, w) for torch tensors: x N x H x W x Cin, w KH x KW x Cin x Cout
+    (both contiguous, same dtype, on the current device); returns y N x OH x OW x Cout."""
+    import torch
+    if x.dim() != 4 or w.dim() != 4 or x.shape[3] != w.shape[2] or x.dtype != w.dtype:
+        raise ValueError("conv2d: x must be N x H x W x Cin, w KH x KW x Cin x Cout, same dtype")
+    if not (x.is_contiguous() and w.is_contiguous()):
+        raise ValueError("conv2d: operands must be contiguous")
+    N, H, W, Cin = x.shape
+    KH, KW, _, Cout = w.shape
+    span_h = H + 2 * padding[0] - dilation[0] * (KH - 1) - 1
+    span_w = W + 2 * padding[1] - dilation[1] * (KW - 1) - 1
+    OH = span_h // stride[0] + 1 if span_h >= 0 else 0
+    OW = span_w // stride[1] + 1 if span_w >= 0 else 0
+    if out is None:
+        out = torch.empty((N, OH, OW, Cout), dtype=x.dtype, device=x.device)
+    d = conv_desc(N, H, W, Cin, Cout, KH, KW, _torch_dtype_code(x), stride, padding, dilation)
+    _chk(vx_conv2d(d, x.data_ptr(), w.data_ptr(), out.data_ptr(), _stream_ptr(stream)), "vx_conv2d")
+    return out

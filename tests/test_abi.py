@@ -298,7 +298,7 @@ def test_fix_wavefront_restricts_the_argmin(mi355x_override):
     assert vx.vx_fix_wavefront(32, 0, 16) == 1
     assert vx.vx_fix_wavefront(-32, 32, 16) == 1
     assert vx.vx_fix_wavefront(24, 24, 16) == 3
-    reg = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]
+    reg = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count())) if k.op == 0]
 
     def wave(k):
         return (k.mb // k.wm, k.nb // k.wn, k.mfma_m)
@@ -359,3 +359,26 @@ def test_backend_restriction(mi355x_override):
         assert vx.vx_restrict_backends(0) == 0
     p = vx.vx_plan_query(1, 3, 1024, 1024, vx.VX_BF16)
     assert p.kernel_id >= 0
+
+
+def test_conv2d_argument_checks_and_plan(mi355x_override):
+    """Host-side checks of the convolution entry point (no device needed) and
+    its plan: a convolution kernel chosen for the implicit-GEMM shape."""
+    d = vx.conv_desc(2, 14, 15, 8, 16, 3, 3, vx.VX_BF16, (2, 1), (1, 1), (1, 2))
+    p = vx.vx_conv2d_plan_query(d)
+    assert p.kernel.op == 1 and p.kernel.vec == 0
+    oh = (14 + 2 - 2 - 1) // 2 + 1
+    ow = (15 + 2 - 4 - 1) // 1 + 1
+    assert p.tiles_m * p.kernel.mb >= 2 * oh * ow and p.tiles_n * p.kernel.nb >= 16
+    bad = [dict(kh=0), dict(stride_h=0), dict(dil_w=0), dict(pad_h=-1), dict(n=-1), dict(c_in=-2)]
+    for b in bad:
+        e = vx.conv_desc(2, 14, 15, 8, 16, 3, 3, vx.VX_BF16, (2, 1), (1, 1), (1, 2))
+        for k, v in b.items():
+            setattr(e, k, v)
+        assert vx.vx_conv2d(e, 16, 4096, 1 << 20) == 1, b
+    e = vx.conv_desc(2, 14, 15, 8, 16, 3, 3, 7)
+    assert vx.vx_conv2d(e, 16, 4096, 1 << 20) == 2                    # unsupported dtype
+    assert vx.vx_conv2d(d, None, 4096, 1 << 20) == 1                  # NULL image with a non-empty extent
+    assert vx.vx_conv2d(d, 16, 4096, 20) == 1                         # y overlaps x
+    empty = vx.conv_desc(2, 2, 2, 8, 16, 5, 5, vx.VX_F16)            # the filter does not fit: no output
+    assert vx.vx_conv2d(empty, None, None, None) == 0
