@@ -43,8 +43,9 @@ def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--workload", default="sweep",
-                    choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single", "mixed"],
-                    help="sweep (default, the headline metric) or one of the other GEMM sets")
+                    choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single", "mixed", "conv"],
+                    help="sweep (default, the headline metric), one of the other GEMM sets, or the "
+                         "dynamic-shape convolution set")
     ap.add_argument("--trials", type=int, default=None, help="trials of a GEMM set (default: the full set)")
     ap.add_argument("--adapt", action="store_true",
                     help="hardware-adaptation study (Section 7.4): fp16, N in {1024, 2048, 4096}, K = 1024, "
@@ -56,7 +57,8 @@ def _parse():
     ap.add_argument("--no-calibration", action="store_true",
                     help="ablation: plan with the purely analytical cost model (ignore the calibration table)")
     ap.add_argument("--compare-torch", action="store_true",
-                    help="also time torch.matmul on each GEMM of a set (context only)")
+                    help="also time torch.matmul (torch's conv2d, channels-last, for the convolution set) "
+                         "on each shape of a set (context only)")
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--m-max", type=int, default=512, help="sweep M = 1..m_max")
@@ -443,6 +445,127 @@ def run_adapt(args):
     print(json.dumps(out), flush=True)
 
 
+def run_conv(args):
+    """Times every layer of the convolution set (fp16, NHWC image, KH x KW x Cin
+    x Cout filter) over rotating HBM-resident copies: TFLOP/s (2 M N K of the
+    implicit GEMM, M = N OH OW, N = Cout, K = KH KW Cin) and the fraction of
+    each layer's roofline, with the compulsory bytes image + filter + output."""
+    import numpy as np
+    import torch
+    from paper_2409_01075_amd import inputs as I
+    from paper_2409_01075_amd import vx
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = vx.lib()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    torch.cuda._sleep(1000000)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    cycles_per_ms = 1e6 / max(e0.elapsed_time(e1), 1e-3)
+    f16 = torch.float16
+    results = []
+    for t in range(40 if args.trials is None else args.trials):
+        Nb, H, W, Cin, Cout, F, st, pd = I.conv_trial(t)
+        d = vx.conv_desc(Nb, H, W, Cin, Cout, F, F, vx.VX_F16, (st, st), (pd, pd))
+        OH = (H + 2 * pd - F) // st + 1
+        OW = (W + 2 * pd - F) // st + 1
+        M, N, K = Nb * OH * OW, Cout, F * F * Cin
+        x = I.device_normal((Nb, H, W, Cin), 1.0, 1000 * t, dev, f16)
+        w = I.device_normal((F, F, Cin, Cout), 0.05, 1000 * t + 1, dev, f16)
+        sx, sw, sy = x.numel() * 2, w.numel() * 2, M * N * 2
+        set_bytes = sx + sw + sy
+        R = int(min(max(2, -(-args.rot_mib * 2 ** 20 // set_bytes)), 4096))
+        px = x.reshape(1, -1).expand(R, -1).contiguous()
+        pw = w.reshape(1, -1).expand(R, -1).contiguous()
+        py = torch.empty((R, M * N), dtype=f16, device=dev)
+        x0, w0, y0 = px.data_ptr(), pw.data_ptr(), py.data_ptr()
+        db = ctypes.byref(d)
+
+        def call(r):
+            return L.vx_conv2d(db, x0 + r * sx, w0 + r * sw, y0 + r * sy, sp)
+        rc = call(0)
+        if rc != 0:
+            raise RuntimeError("conv trial %d: %s" % (t, vx.STATUS.get(rc, rc)))
+        torch.cuda.synchronize()
+        times = []
+        n_calls = max(R, 8)
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(int(cycles_per_ms * 0.3))
+            e0.record(stream)
+            for i in range(n_calls):
+                call(i % R)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / n_calls * 1e-3)
+        tm = float(np.median(times))
+        plan = vx.vx_conv2d_plan_query(d)
+        flops = 2.0 * M * N * K
+        t_mfma = flops / (MFMA_PEAK_TFLOPS[1] * 1e12)
+        t_hbm = set_bytes / (HBM_PEAK_GBPS * 1e9)
+        r = {"trial": t, "layer": [Nb, H, W, Cin, Cout, F, st, pd], "M": M, "N": N, "K": K,
+             "bytes": set_bytes, "us": tm * 1e6, "tflops": flops / tm / 1e12, "gbps": set_bytes / tm / 1e9,
+             "bound": "mfma" if t_mfma >= t_hbm else "hbm", "roof_frac": max(t_mfma, t_hbm) / tm,
+             "kernel": plan.kernel_id, "split": plan.split_k,
+             "tile": [plan.kernel.mb, plan.kernel.nb, plan.kernel.kb]}
+        if args.compare_torch:
+            xt = x.permute(0, 3, 1, 2)                                   # NCHW view of the NHWC image
+            wt = w.permute(3, 2, 0, 1).contiguous(memory_format=torch.channels_last)
+            fn = torch.nn.functional.conv2d
+            fn(xt, wt, None, st, pd)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(8):
+                fn(xt, wt, None, st, pd)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            r["torch_us"] = e0.elapsed_time(e1) / 8 * 1e3
+        results.append(r)
+        print("conv t%-3d %-36s M %7d N %4d K %6d %9.1f us %7.1f TFLOP/s %6.0f GB/s %s %5.1f%% of roof "
+              "kid %d split %d%s" % (t, str(r["layer"]), M, N, K, r["us"], r["tflops"], r["gbps"], r["bound"],
+                                     100 * r["roof_frac"], r["kernel"], r["split"],
+                                     ("  torch %.1f us" % r["torch_us"]) if "torch_us" in r else ""),
+              file=sys.stderr, flush=True)
+        del px, pw, py, x, w
+
+    def geo(v):
+        v = [x for x in v if x > 0]
+        return float(np.exp(np.mean(np.log(v)))) if v else None
+    by_kernel = {}
+    for r in results:
+        by_kernel.setdefault(r["kernel"], []).append(r)
+    kid = max(by_kernel, key=lambda k: sum(r["us"] for r in by_kernel[k]))
+    dom = by_kernel[kid]
+    dom_t = sum(r["us"] for r in dom) * 1e-6
+    if sum(r["us"] for r in dom if r["bound"] == "hbm") > dom_t * 5e5:
+        ach = sum(r["bytes"] for r in dom) / dom_t / 1e9
+        roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBPS}
+    else:
+        ach = sum(2.0 * r["M"] * r["N"] * r["K"] for r in dom) / dom_t / 1e12
+        roof = {"bound": "mfma", "achieved": ach, "peak": MFMA_PEAK_TFLOPS[1], "unit": "TFLOP/s",
+                "frac": ach / MFMA_PEAK_TFLOPS[1]}
+    roof.update({"traffic": None, "kernel": "vxk_%d" % kid, "launches": len(dom),
+                 "avg_us": dom_t / len(dom) * 1e6})
+    out = {"metric": "Conv TFLOP/s geomean over a dynamic-shape CNN convolution set; % of MFMA/HBM roofline",
+           "value": geo([r["tflops"] for r in results]), "unit": "TFLOP/s", "n_gpus": 1, "steps": 1,
+           "warmup": 1, "ms_per_step": sum(r["us"] for r in results) / 1e3, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic (seeded, on device)",
+           "config": {"workload": "dynamic-shape convolution set: fp16 NHWC layers of the CNN ranges of Table 4",
+                      "layers": len(results)},
+           "roofline": roof, "roof_frac_geomean": geo([r["roof_frac"] for r in results])}
+    if args.compare_torch:
+        out["vs_torch_conv2d_geomean"] = geo([r["torch_us"] / r["us"] for r in results])
+    if args.detail:
+        with open(args.detail, "w") as f:
+            json.dump(results, f)
+    out["selector"] = _selector_kind()
+    print(json.dumps(out), flush=True)
+
+
 def run_set(args):
     """Times every GEMM of a set over rotating HBM-resident copies and reports
     TFLOP/s and the fraction of each shape's roofline."""
@@ -578,6 +701,9 @@ def main():
         return
     if args.adapt:
         run_adapt(args)
+        return
+    if args.workload == "conv":
+        run_conv(args)
         return
     if args.workload != "sweep":
         run_set(args)

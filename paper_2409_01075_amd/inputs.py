@@ -25,6 +25,16 @@ sizes listed below; the paper's own benchmark items are not reproduced):
 * ``llm_trial(t)``  bf16, seed t: M = clip(floor(exp(U[0, ln 8193))), 1, 8192);
   (M,4096)x(4096,4096), (M,4096)x(4096,11008), (M,11008)x(11008,4096);
   activations N(0,1), weights N(0,0.02).
+* ``conv_trial(t)``  fp16, seed 5000 + t: one convolution layer drawn inside
+  the ranges of the paper's CNN convolution family (Table 4: batch 1..64,
+  feature map 4..768, filter 1..11, Cin 3..832, Cout 16..512).  Filter F from
+  {1, 3, 5, 7, 11} with weights (.35, .45, .08, .07, .05); a 7 x 7 or 11 x 11
+  filter is a stem layer (Cin = 3) half of the time; Cin = 8 round(e^U[ln 2,
+  ln 104]) otherwise, Cout = 16 round(e^U[0, ln 32]); stride 2 with
+  probability 1/4 (4 for an 11 x 11 stem); padding F // 2; feature map
+  round(e^U[ln 4, ln 768]) and batch round(e^U[0, ln 64]), halved (batch
+  first, then the map) until the layer holds at most 2^25 input and 2^25
+  output elements and 4e11 flops.  Images N(0, 1), filters N(0, 0.05).
 * ``small_int`` helpers: integer-valued operands whose every partial sum is
   exact in fp32 and whose result is exact in the output type.
 """
@@ -36,6 +46,10 @@ ENCODER_SHAPES = [(768, 2304), (768, 768), (768, 3072), (3072, 768)]   # (K, N) 
 LLM_SHAPES = [(4096, 4096), (4096, 11008), (11008, 4096)]              # (K, N) per GEMM
 ATTN_BATCH = 16 * 12
 ATTN_HEAD = 64
+
+
+CONV_FILTERS = (1, 3, 5, 7, 11)
+CONV_FILTER_P = (0.35, 0.45, 0.08, 0.07, 0.05)
 
 
 def rng(seed):
@@ -175,3 +189,32 @@ def exact_range(K, dtype):
     p = {F32: 24, F16: 11, BF16: 8}[code_of(dtype)]
     r = int(np.floor(np.sqrt((2.0 ** p) / max(K, 1))))
     return max(r, 0)
+
+
+def conv_trial(t):
+    """(N, H, W, Cin, Cout, F, stride, pad) of convolution trial t (fp16, square
+    filter and map, dilation 1)."""
+    g = rng(5000 + t)
+    F = int(g.choice(CONV_FILTERS, p=CONV_FILTER_P))
+    stem = F >= 7 and g.random() < 0.5
+    Cin = 3 if stem else 8 * int(round(np.exp(g.uniform(np.log(2), np.log(104)))))
+    Cout = 16 * int(round(np.exp(g.uniform(0.0, np.log(32)))))
+    stride = (4 if F == 11 else 2) if (stem or g.random() < 0.25) else 1
+    pad = F // 2
+    H = int(round(np.exp(g.uniform(np.log(4), np.log(768)))))
+    N = int(round(np.exp(g.uniform(0.0, np.log(64)))))
+
+    def size(N, H):
+        OH = (H + 2 * pad - F) // stride + 1
+        return N * H * H * Cin, N * OH * OH * Cout, 2.0 * N * OH * OH * Cout * F * F * Cin
+    while True:
+        xi, yo, fl = size(N, H)
+        if xi <= 2 ** 25 and yo <= 2 ** 25 and fl <= 4e11:
+            break
+        if N > 1:
+            N //= 2
+        else:
+            H = max(H // 2, F)
+            if H == F:
+                break
+    return N, H, H, Cin, Cout, F, stride, pad
