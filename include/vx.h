@@ -251,7 +251,8 @@ vx_status vx_set_workspace(void* ptr, size_t bytes, void* stream);
  * allowed): x n x h x w x c_in, w kh x kw x c_in x c_out, y n x oh x ow x
  * c_out.  fp32 accumulation; y rounded to nearest even in `dtype`.
  * Ownership and errors as for vx_gemm: sizes < 0, kh/kw/strides/dilations
- * < 1, pads < 0, extents beyond 32-bit element counts, a NULL operand with a
+ * < 1, pads < 0, h + 2*pad_h or w + 2*pad_w of 2^30 or more, M, K, M*c_out
+ * or K*c_out beyond 2^31 - 1 elements, a NULL operand with a
  * non-empty extent, or y overlapping x or w -> VX_ERR_INVALID_ARG; an empty
  * output is a no-op; c_in = 0 writes zeros.  Asynchronous on `stream`.
  */

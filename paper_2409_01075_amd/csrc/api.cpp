@@ -397,8 +397,9 @@ vx_status conv_shape(const vx_conv2d_desc* d, VxShape* sh, VxGemmArgs* a, bool* 
     if (d->n < 0 || d->h < 0 || d->w < 0 || d->c_in < 0 || d->c_out < 0 || d->kh < 1 || d->kw < 1 ||
         d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0 || d->dil_h < 1 || d->dil_w < 1)
         return VX_ERR_INVALID_ARG;
-    const int64_t lim = INT32_MAX;
-    if (d->h > lim || d->w > lim || d->kh > lim || d->kw > lim || d->pad_h > lim / 4 || d->pad_w > lim / 4 ||
+    const int64_t lim = INT32_MAX, span_lim = (int64_t)1 << 30;
+    if (d->h >= span_lim || d->w >= span_lim || d->pad_h >= span_lim || d->pad_w >= span_lim ||
+        d->h + 2 * d->pad_h >= span_lim || d->w + 2 * d->pad_w >= span_lim || d->kh > lim || d->kw > lim ||
         d->stride_h > lim || d->stride_w > lim || d->dil_h > lim || d->dil_w > lim)
         return VX_ERR_INVALID_ARG;
     const int64_t oh = conv_out_dim(d->h, d->kh, d->stride_h, d->pad_h, d->dil_h);

@@ -196,52 +196,65 @@ struct Tile {
     // gk = (kh * KW + kw) * Cin + ci.  When Cin is a multiple of the chunk,
     // a chunk never straddles two taps and is one 16-byte load (or zeros in
     // the padding); otherwise it is gathered element by element.
-    __device__ __forceinline__ void load_a_conv(const VxGemmArgs& p, const char* __restrict__ X, int m0, int k0,
-                                                int kend, int t)
+    // A of a convolution: the K step at the chunk column held in `ca` (see
+    // ConvA), gathered through the im2col map; taps in the padding and k at or
+    // past kend read as zeros.
+    template <class CA>
+    __device__ __forceinline__ void load_a_conv(const VxGemmArgs& p, const char* __restrict__ X, const CA& ca,
+                                                int kend)
     {
-        const bool whole = p.cC % C::VE == 0;   // wave-uniform
+        if (p.cC % C::VE == 0) {   // wave-uniform: a chunk is VE channels of one tap
+            const int dh = ca.kh * p.cdh, dw = ca.kw * p.cdw;
+            const int64_t koff = ((int64_t)dh * p.cW + dw) * p.cC + ca.ci;
+            const bool kin = ca.gk < kend;
+#pragma unroll
+            for (int v = 0; v < C::AV; ++v) {
+                u32x4 x = {0, 0, 0, 0};
+                if (kin && (unsigned)(ca.ih0[v] + dh) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dw) < (unsigned)p.cW)
+                    x = *(const u32x4_u*)(X + (ca.pix[v] + koff) * C::EB);
+                ra[v] = x;
+            }
+            return;
+        }
+        // channels not a multiple of the chunk: the VE elements of a chunk walk
+        // over channels, then filter columns, then filter rows
+        int ci = ca.ci, kw = ca.kw, kh = ca.kh;
+        int dhe[C::VE], dwe[C::VE];
+        int64_t koff[C::VE];
+#pragma unroll
+        for (int e = 0; e < C::VE; ++e) {
+            dhe[e] = ca.gk + e < kend ? kh * p.cdh : -(1 << 30);   // k past kend: an out-of-range row
+            dwe[e] = kw * p.cdw;
+            koff[e] = ((int64_t)(kh * p.cdh) * p.cW + dwe[e]) * p.cC + ci;
+            if (++ci == p.cC) {
+                ci = 0;
+                if (++kw == p.cKW) {
+                    kw = 0;
+                    ++kh;
+                }
+            }
+        }
 #pragma unroll
         for (int v = 0; v < C::AV; ++v) {
-            const int idx = t + v * C::NT;
-            const int r = idx / (C::KB / C::VE), c = idx % (C::KB / C::VE);
-            const int gm = m0 + r, gk = k0 + c * C::VE;
-            u32x4 x = {0, 0, 0, 0};
-            if (gm < p.M && gk < kend) {
-                const int ow = gm % p.cOW, q = gm / p.cOW;
-                const int oh = q % p.cOH, n = q / p.cOH;
-                const int ih0 = oh * p.csh - p.cph, iw0 = ow * p.csw - p.cpw;
-                if (whole) {
-                    const int ci = gk % p.cC, khw = gk / p.cC;
-                    const int ih = ih0 + (khw / p.cKW) * p.cdh, iw = iw0 + (khw % p.cKW) * p.cdw;
-                    if (ih >= 0 && ih < p.cH && iw >= 0 && iw < p.cW)
-                        x = *(const u32x4_u*)(X + (((int64_t)n * p.cH + ih) * p.cW + iw) * (int64_t)p.cC * C::EB +
-                                              (int64_t)ci * C::EB);
-                } else {
-                    unsigned e16[C::VE];
+            unsigned e16[C::VE];
 #pragma unroll
-                    for (int e = 0; e < C::VE; ++e) {
-                        const int k = gk + e;
-                        unsigned val = 0u;
-                        if (k < kend) {
-                            const int ci = k % p.cC, khw = k / p.cC;
-                            const int ih = ih0 + (khw / p.cKW) * p.cdh, iw = iw0 + (khw % p.cKW) * p.cdw;
-                            if (ih >= 0 && ih < p.cH && iw >= 0 && iw < p.cW) {
-                                const char* src = X + ((((int64_t)n * p.cH + ih) * p.cW + iw) * p.cC + ci) * C::EB;
-                                val = C::H ? (unsigned)*(const uint16_t*)src : *(const unsigned*)src;
-                            }
-                        }
-                        e16[e] = val;
-                    }
-                    if (C::H) {
-#pragma unroll
-                        for (int e = 0; e < 8; e += 2)
-                            x[e >> 1] = pack2(e16[e], e16[e + 1]);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            x[e] = e16[e];
-                    }
+            for (int e = 0; e < C::VE; ++e) {
+                unsigned val = 0u;
+                if ((unsigned)(ca.ih0[v] + dhe[e]) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dwe[e]) < (unsigned)p.cW) {
+                    const char* src = X + (ca.pix[v] + koff[e]) * C::EB;
+                    val = C::H ? (unsigned)*(const uint16_t*)src : *(const unsigned*)src;
                 }
+                e16[e] = val;
+            }
+            u32x4 x;
+            if (C::H) {
+#pragma unroll
+                for (int e = 0; e < 8; e += 2)
+                    x[e >> 1] = pack2(e16[e], e16[e + 1]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    x[e] = e16[e];
             }
             ra[v] = x;
         }
@@ -734,6 +747,64 @@ __device__ __forceinline__ void store_lds(const VxGemmArgs& p, Acc<C>& acc, cons
 // ------------------------------------------------- register-staged family --
 // Level 1 with loads staged through VGPRs (any dtype; 16-bit B is transposed
 // in registers on its way into LDS).
+// Per-thread im2col state of a convolution's A operand (the implicit GEMM's
+// M x K matrix, row m = output pixel (n, oh, ow), column k = (kh, kw, ci) of
+// the KH x KW x Cin filter).  A thread loads the same chunk column c of every
+// K step in AV rows; the row part of each address (image n, top-left tap
+// ih0, iw0) is fixed for the whole kernel and computed once, and the column
+// part (ci, kw, kh of the chunk's first k) advances by KB per step.  Rows past
+// M get ih0 = -2^30, so that every tap of theirs tests out of range (the
+// host keeps H + 2 pad and W + 2 pad below 2^30, hence also the filter span
+// of any convolution with a non-empty output).
+template <class C>
+struct ConvA {
+    static constexpr int CPR = C::KB / C::VE;   // chunks per row of a K step
+    static_assert(!C::CONV || C::NT % CPR == 0, "a thread's chunk column is the same in each of its rows");
+    int64_t pix[C::AV];                         // element offset of (n, ih0, iw0), may be negative
+    int ih0[C::AV], iw0[C::AV];
+    int gk, ci, kw, kh;                         // first k of the chunk, and its (ci, kw, kh)
+
+    __device__ __forceinline__ void init(const VxGemmArgs& p, int m0, int kbeg, int t)
+    {
+#pragma unroll
+        for (int v = 0; v < C::AV; ++v) {
+            const int gm = m0 + (t + v * C::NT) / CPR;
+            const int ow = gm % p.cOW, q = gm / p.cOW;
+            const int oh = q % p.cOH, n = q / p.cOH;
+            const bool in = gm < p.M;
+            ih0[v] = in ? oh * p.csh - p.cph : -(1 << 30);
+            iw0[v] = in ? ow * p.csw - p.cpw : 0;
+            pix[v] = (((int64_t)n * p.cH + ih0[v]) * p.cW + iw0[v]) * p.cC;
+        }
+        gk = kbeg + (t % CPR) * C::VE;
+        decompose(p);
+    }
+    __device__ __forceinline__ void decompose(const VxGemmArgs& p)
+    {
+        ci = gk % p.cC;
+        const int khw = gk / p.cC;
+        kw = khw % p.cKW;
+        kh = khw / p.cKW;
+    }
+    // on to the next K step
+    __device__ __forceinline__ void advance(const VxGemmArgs& p)
+    {
+        gk += C::KB;
+        if (C::KB <= p.cC) {                    // wave-uniform; one wrap at most
+            ci += C::KB;
+            if (ci >= p.cC) {
+                ci -= p.cC;
+                if (++kw == p.cKW) {
+                    kw = 0;
+                    ++kh;
+                }
+            }
+        } else {
+            decompose(p);
+        }
+    }
+};
+
 template <class C>
 __device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
 {
@@ -755,11 +826,17 @@ __device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
     acc_zero<C>(acc);
 
     Tile<C> tl;
-    // one K step of A and B into registers (for a convolution, A through the im2col map)
+    ConvA<C> ca;
+    if constexpr (C::CONV)
+        ca.init(p, g.m0, g.kbeg, t);
+    // one K step of A and B into registers (for a convolution, A through the
+    // im2col map; the steps come in order, so its state just advances)
     auto load = [&](int k0) {
         tl.load(Ab, Bb, 0, g.n0, k0, g.kend, Mrel, p.N, p.K, t);
-        if constexpr (C::CONV)
-            tl.load_a_conv(p, (const char*)p.A, g.m0, k0, g.kend, t);
+        if constexpr (C::CONV) {
+            tl.load_a_conv(p, (const char*)p.A, ca, g.kend);
+            ca.advance(p);
+        }
     };
     if (g.nk > 0) {
         load(g.kbeg);

@@ -382,3 +382,15 @@ def test_conv2d_argument_checks_and_plan(mi355x_override):
     assert vx.vx_conv2d(d, 16, 4096, 20) == 1                         # y overlaps x
     empty = vx.conv_desc(2, 2, 2, 8, 16, 5, 5, vx.VX_F16)            # the filter does not fit: no output
     assert vx.vx_conv2d(empty, None, None, None) == 0
+
+
+def test_conv2d_extent_limits(mi355x_override):
+    """Padded image extents of 2^30 or more are rejected (the kernels keep tap
+    coordinates in 32 bits with a -2^30 sentinel for rows past M)."""
+    for kw in (dict(h=(1 << 30) - 2, pad_h=1), dict(w=(1 << 29), pad_w=(1 << 28)), dict(pad_w=1 << 30)):
+        d = vx.conv_desc(1, 4, 4, 8, 8, 1, 1, vx.VX_F16)
+        for k, v in kw.items():
+            setattr(d, k, v)
+        assert vx.vx_conv2d(d, 16, 1 << 40, 1 << 41) == 1, kw
+    d = vx.conv_desc(1, (1 << 30) - 3, 1, 8, 1, 1, 1, vx.VX_F16, pad=(1, 0))
+    assert vx.vx_conv2d_plan_query(d).kernel.op == 1
