@@ -416,7 +416,11 @@ vx_status conv_shape(const vx_conv2d_desc* d, VxShape* sh, VxGemmArgs* a, bool* 
     sh->N = d->c_out;
     sh->K = (int64_t)K;
     sh->dt = d->dtype;
-    sh->vec_ok = 0;   // the conv kernels take element-aligned operands
+    // 16-byte chunks of 8 channels for the direct-to-LDS kernels, whose
+    // image offsets are 32-bit (operand alignment is checked by the caller
+    // that has the pointers); vec_ok is part of the plan cache's key
+    sh->a_bytes = (int64_t)((double)d->n * d->h * d->w * d->c_in) * elem_bytes(d->dtype);
+    sh->vec_ok = d->dtype != VX_F32 && d->c_in % 8 == 0 && d->c_out % 8 == 0 && sh->a_bytes < ((int64_t)1 << 31);
     sh->c_vec = 0;
     sh->op = 1;
     a->cH = (int)d->h;
@@ -569,6 +573,7 @@ vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void*
         return VX_ERR_INVALID_ARG;
     if (empty)
         return VX_OK;
+    sh.vec_ok = sh.vec_ok && (uintptr_t)x % 16 == 0 && (uintptr_t)w % 16 == 0;
     a.A = x;
     a.B = w;
     a.C = y;

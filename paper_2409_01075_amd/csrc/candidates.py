@@ -261,6 +261,31 @@ def conv_candidates(dtype, hw=GFX950):
     return out
 
 
+# fp16/bf16 convolutions whose channel counts are multiples of 8 (and whose
+# image fits 32-bit buffer offsets) also get direct-to-LDS tiles: each lane's
+# 16-byte chunk is one tap's 8 channels, fetched with its own buffer offset,
+# and a tap in the padding gets an out-of-range offset that reads as zeros.
+# Kb = 64 (one 128-byte row segment per 8 lanes keeps a lane's chunk column
+# fixed); 4 waves below 128 x 128, 8 from there up to 256 x 128 (256 x 256
+# spills with the map state); wave tiles at most 2:1; the 2-stage ring and
+# the deepest ring of at most 4 stages.
+def conv_dma_candidates(dtype, hw=GFX950):
+    out = []
+    for c in generate_candidates_for_layer(2, dtype, hw, "dma")[0]:
+        mb, nb, kb, wm, wn, mi = c
+        mw, nw = mb // wm, nb // wn
+        if kb != 64 or min(mb, nb) < 64 or mb * nb > 256 * 128 or wm * wn != (8 if mb * nb >= 128 * 128 else 4):
+            continue
+        if max(mw, nw) > 2 * min(mw, nw):
+            continue
+        st = dma_stage_options(*c, 1, hw)
+        for s in sorted({st[0], max(x for x in st if x <= 4)}):
+            e = _entry(dtype, "dma", s, c, 1, hw)
+            e["op"] = 1
+            out.append(e)
+    return out
+
+
 # ------------------------------------------------- vector-ALU family (L0') --
 # The adaptive second backend for small M (the paper's CUDA-core path next to
 # the tensor-core path): level 0 is one lane's MT x VE outputs computed with
@@ -323,6 +348,8 @@ def registry(hw=GFX950):
         out += valu_candidates(dtype, hw)
     for dtype in ("f16", "bf16", "f32"):
         out += conv_candidates(dtype, hw)
+    for dtype in ("f16", "bf16"):
+        out += conv_dma_candidates(dtype, hw)
     for i, e in enumerate(out):
         e["id"] = i
     return out

@@ -26,10 +26,11 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
-template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_>
+template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_, bool CONV_ = false>
 struct DCfg {
     static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_, STAGES = ST_;
     static constexpr bool VEC = VEC_;
+    static constexpr bool CONV = CONV_;   // A is an image read through the im2col map
     static constexpr bool H = true;
     static constexpr int EB = 2;
     static constexpr int NWAVE = WM * WN, NT = NWAVE * 64;
@@ -64,6 +65,7 @@ struct DCfg {
     static_assert(STAGES >= 2 && STAGES <= 16, "pipeline depth");
     static_assert((STAGES - 1) * LPS <= 63, "vmcnt range: the prologue's DMA all in flight");
     static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
+    static_assert(!CONV || CPA == 8, "convolution: one 128-byte row segment per 8 lanes (Kb = 64)");
 };
 
 __device__ __forceinline__ int swz_a(int r, int period) { return r & (period - 1); }
@@ -128,6 +130,63 @@ __device__ __forceinline__ void dma_lds(const u32x4& r, lds_char* dst, unsigned 
                  : "memory");
 }
 
+// Per-lane im2col state of a convolution's A for the direct-to-LDS loads.
+// With Kb = 64 the A instruction I of wave w moves row (w*A_IPW + I)*8 +
+// lane/8 of the tile, always at chunk column (lane%8) ^ swizzle(lane/8): the
+// column part of the map (ci, kw, kh of the chunk's first k) is shared by a
+// lane's A_IPW rows and advances by Kb per K step; the row part (image n,
+// top-left tap ih0, iw0) is fixed.  Element offsets are kept modulo 2^32:
+// every tap that is loaded lies in the image, whose element count the host
+// keeps below 2^30, so the wrapped sum of the row and column parts is exact
+// there.  Rows past M get ih0 = -2^30 (every tap tests out of range; the
+// host keeps H + 2 pad and W + 2 pad below 2^30).
+template <class C>
+struct DmaConvA {
+    unsigned pix[C::A_IPW];   // element offset of (n, ih0, iw0), mod 2^32
+    int ih0[C::A_IPW], iw0[C::A_IPW];
+    int gk, ci, kw, kh;
+
+    __device__ __forceinline__ void init(const VxGemmArgs& p, int m0, int kbeg, int wave, int lane)
+    {
+#pragma unroll
+        for (int i = 0; i < C::A_IPW; ++i) {
+            const int gm = m0 + (wave * C::A_IPW + i) * 8 + lane / 8;
+            const int ow = gm % p.cOW, q = gm / p.cOW;
+            const int oh = q % p.cOH, n = q / p.cOH;
+            const bool in = gm < p.M;
+            ih0[i] = in ? oh * p.csh - p.cph : -(1 << 30);
+            iw0[i] = in ? ow * p.csw - p.cpw : 0;
+            pix[i] = (((unsigned)n * (unsigned)p.cH + (unsigned)ih0[i]) * (unsigned)p.cW + (unsigned)iw0[i]) *
+                     (unsigned)p.cC;
+        }
+        gk = kbeg + ((lane % 8) ^ ((lane / 8) % 8)) * 8;
+        decompose(p);
+    }
+    __device__ __forceinline__ void decompose(const VxGemmArgs& p)
+    {
+        ci = gk % p.cC;
+        const int khw = gk / p.cC;
+        kw = khw % p.cKW;
+        kh = khw / p.cKW;
+    }
+    __device__ __forceinline__ void advance(const VxGemmArgs& p)
+    {
+        gk += C::KB;
+        if (C::KB <= p.cC) {   // wave-uniform; one wrap at most
+            ci += C::KB;
+            if (ci >= p.cC) {
+                ci -= p.cC;
+                if (++kw == p.cKW) {
+                    kw = 0;
+                    ++kh;
+                }
+            }
+        } else {
+            decompose(p);
+        }
+    }
+};
+
 template <class C>
 struct DmaTile {
     // The DMA of one K step (starting at k0) into one LDS stage: LPS
@@ -137,6 +196,12 @@ struct DmaTile {
     lds_char* stage;
     u32x4 ra, rb;   // A resource at column k0 of the panel; B resource at row k0, column n0
     int kv, nv;     // valid columns of A from k0; valid columns of B from n0
+    // convolution: the image's resource in ra, and this step's column part of
+    // the im2col map (filter row and column offsets, element offset mod 2^32)
+    const DmaConvA<C>* cv = nullptr;
+    int dh = 0, dw = 0, cH = 0, cW = 0;
+    unsigned koff = 0;
+    bool kin = false;
 
     __device__ __forceinline__ DmaTile(lds_char* stage_, const char* Apanel, const char* Bbatch, int k0, int kend, int n0,
                                        int N)
@@ -145,10 +210,25 @@ struct DmaTile {
     {
     }
 
+    // Convolution step: A from the image X through the map state `c` (whose
+    // column part describes this step's k0).
+    __device__ __forceinline__ DmaTile(lds_char* stage_, const char* X, const char* Bbatch, int k0, int kend, int n0,
+                                       const VxGemmArgs& p, const DmaConvA<C>& c)
+        : stage(stage_), ra(buffer_rsrc(X, kOOB)), rb(buffer_rsrc(Bbatch + ((int64_t)k0 * p.N + n0) * 2, kOOB)),
+          kv(kend - k0), nv(p.N - n0), cv(&c), dh(c.kh * p.cdh), dw(c.kw * p.cdw), cH(p.cH), cW(p.cW),
+          koff(((unsigned)dh * (unsigned)p.cW + (unsigned)dw) * (unsigned)p.cC + (unsigned)c.ci), kin(c.gk < kend)
+    {
+    }
+
     template <int I>
     __device__ __forceinline__ void one(int Mrel, int N, int K, int wave, int lane) const
     {
-        if constexpr (I < C::A_IPW) {
+        if constexpr (I < C::A_IPW && C::CONV) {
+            // A: the taps of this lane's output pixel I at this step's columns
+            const int instr = wave * C::A_IPW + I;
+            const bool ok = kin && (unsigned)(cv->ih0[I] + dh) < (unsigned)cH && (unsigned)(cv->iw0[I] + dw) < (unsigned)cW;
+            dma_lds<C::LANE_BYTES>(ra, stage + instr * C::WAVE_BYTES, ok ? (cv->pix[I] + koff) * 2u : kOOB);
+        } else if constexpr (I < C::A_IPW) {
             // A: rows of the workgroup's panel
             const int instr = wave * C::A_IPW + I;
             const int slot = instr * 64 + lane;                  // chunk index in the stage
@@ -278,7 +358,9 @@ __device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm
 template <class C>
 __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
 {
-    const VxGemmArgs p = pin_args(args);
+    VxGemmArgs p = pin_args(args);
+    if constexpr (C::CONV)
+        pin_conv(p);
     // The ring: STAGES stages of one K step each.  Stage indices are
     // compile-time constants in the unrolled main loop below.
     constexpr int SB = C::STAGE_BYTES;
@@ -303,11 +385,24 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
     // full, STAGES-2 steps stay in flight behind the one waited for; in the
     // last STAGES-2 iterations (the drain) the count falls to 0.
     // prologue: the first min(STAGES-1, nk) K steps, step s into stage s
+    DmaConvA<C> cv;
+    if constexpr (C::CONV)
+        cv.init(p, g.m0, g.kbeg, wave, lane);
+    // the DMA of the K step at k0 into stage st (for a convolution, at the
+    // map state's step, which then moves on: steps are made in order)
+    auto tile = [&](lds_char* st, int k0) {
+        if constexpr (C::CONV) {
+            const DmaTile<C> d(st, (const char*)p.A, Bbatch, k0, g.kend, g.n0, p, cv);
+            cv.advance(p);
+            return d;
+        } else {
+            return DmaTile<C>(st, Apanel, Bbatch, k0, g.kend, g.n0, p.N);
+        }
+    };
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s)
         if (s < g.nk)
-            DmaTile<C>(VX_STAGE(s), Apanel, Bbatch, g.kbeg + s * C::KB, g.kend, g.n0, p.N).issue(Mrel, p.N, p.K, wave,
-                                                                                                   lane);
+            tile(VX_STAGE(s), g.kbeg + s * C::KB).issue(Mrel, p.N, p.K, wave, lane);
     // main loop, unrolled by STAGES so that every stage index is a constant
     for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
 #pragma unroll
@@ -318,8 +413,7 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
             wait_steps<C::LPS, C::STAGES - 2>(g.nk - 1 - it);   // step `it` has landed (this wave's part)
             __builtin_amdgcn_s_barrier();                      // ... and every wave's; stage it-1 is free
             // step it+STAGES-1 goes into the freed stage, issued between the MFMAs of step it
-            const DmaTile<C> next(VX_STAGE((j + C::STAGES - 1) % C::STAGES), Apanel, Bbatch,
-                                  g.kbeg + (it + C::STAGES - 1) * C::KB, g.kend, g.n0, p.N);
+            const DmaTile<C> next = tile(VX_STAGE((j + C::STAGES - 1) % C::STAGES), g.kbeg + (it + C::STAGES - 1) * C::KB);
             dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, next, it + C::STAGES - 1 < g.nk, Mrel, p.N, p.K, wave);
         }
     }

@@ -104,8 +104,10 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     }
     if (k.family == 1) {
         // direct-to-LDS kernels address each K step with 32-bit buffer offsets:
-        // Mb rows of A (Mb*K elements) and Kb rows of B (Kb*N elements)
-        if ((double)k.mb * sh.K * eb >= 2147483648.0 || (double)k.kb * sh.N * eb >= 2147483648.0)
+        // Mb rows of A (Mb*K elements) and Kb rows of B (Kb*N elements); a
+        // convolution's A offsets run over the whole image
+        const double a_span = k.op == 1 ? (double)sh.a_bytes : (double)k.mb * sh.K * eb;
+        if (a_span >= 2147483648.0 || (double)k.kb * sh.N * eb >= 2147483648.0)
             return -1.0;
     }
     if (k.family == 2) {

@@ -40,6 +40,7 @@ struct VxShape {
     int vec_ok;    // operands allow 16-byte vector loads
     int c_vec;     // C allows 4-element vector stores
     int op = 0;    // 0: GEMM; 1: 2-D convolution as an implicit GEMM (conv kernels only)
+    int64_t a_bytes = 0;   // convolution: bytes of the image (the direct-to-LDS kernels need < 2^31)
 };
 
 struct VxLimits {

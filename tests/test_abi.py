@@ -366,7 +366,10 @@ def test_conv2d_argument_checks_and_plan(mi355x_override):
     its plan: a convolution kernel chosen for the implicit-GEMM shape."""
     d = vx.conv_desc(2, 14, 15, 8, 16, 3, 3, vx.VX_BF16, (2, 1), (1, 1), (1, 2))
     p = vx.vx_conv2d_plan_query(d)
-    assert p.kernel.op == 1 and p.kernel.vec == 0
+    assert p.kernel.op == 1
+    # channels not a multiple of 8: the register-staged (element-gathering) kernels only
+    d3 = vx.conv_desc(2, 14, 15, 3, 16, 3, 3, vx.VX_BF16, (2, 1), (1, 1), (1, 2))
+    assert vx.vx_conv2d_plan_query(d3).kernel.vec == 0
     oh = (14 + 2 - 2 - 1) // 2 + 1
     ow = (15 + 2 - 4 - 1) // 1 + 1
     assert p.tiles_m * p.kernel.mb >= 2 * oh * ow and p.tiles_n * p.kernel.nb >= 16
@@ -394,3 +397,15 @@ def test_conv2d_extent_limits(mi355x_override):
         assert vx.vx_conv2d(d, 16, 1 << 40, 1 << 41) == 1, kw
     d = vx.conv_desc(1, (1 << 30) - 3, 1, 8, 1, 1, 1, vx.VX_F16, pad=(1, 0))
     assert vx.vx_conv2d_plan_query(d).kernel.op == 1
+
+
+def test_conv2d_large_image_avoids_32_bit_offsets(mi355x_override):
+    """An image of 2^31 bytes or more is beyond the direct-to-LDS kernels'
+    32-bit buffer offsets: the plan takes a register-staged kernel, which
+    forms 64-bit addresses; below that a direct-to-LDS kernel is planned."""
+    big = vx.conv_desc(1, 1 << 15, 1 << 12, 16, 8, 1, 1, vx.VX_F16)      # 2^31 elements, 2^32 bytes
+    p = vx.vx_conv2d_plan_query(big)
+    assert p.kernel.op == 1 and p.kernel.family == 0
+    small = vx.conv_desc(8, 256, 256, 64, 128, 3, 3, vx.VX_F16, pad=(1, 1))
+    p = vx.vx_conv2d_plan_query(small)
+    assert p.kernel.op == 1 and p.kernel.family == 1

@@ -54,8 +54,10 @@ def test_every_conv_kernel_integer_exact(code):
           if k.op == 1 and k.dtype == code and k.enabled]
     assert ks
     for k in ks:
-        for Cin in (3, 8):
-            N, H, W, Cout, KH, KW, st, pd, dl = 2, 11, 10, k.nb + 5, 3, 3, (2, 1), (1, 2), (1, 2)
+        # the direct-to-LDS kernels take channel counts that are multiples of 8
+        for Cin in ((8, 24) if k.vec else (3, 8)):
+            Cout = k.nb + (8 if k.vec else 5)
+            N, H, W, KH, KW, st, pd, dl = 2, 11, 10, 3, 3, (2, 1), (1, 2), (1, 2)
             x = I.small_int(g, (N, H, W, Cin), code, -3, 3)
             w = I.small_int(g, (KH, KW, Cin, Cout), code, -3, 3)
             assert vx.vx_force_plan(k.id, 1) == 0
@@ -70,13 +72,16 @@ def test_every_conv_kernel_integer_exact(code):
 @pytest.mark.parametrize("code", DTS)
 def test_conv_split_k_integer_exact(code):
     g = I.rng(1300 + code)
-    k = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count()))
-         if k.op == 1 and k.dtype == code and k.enabled][0]
+    conv = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count()))
+            if k.op == 1 and k.dtype == code and k.enabled]
     N, H, W, Cin, Cout, KH, KW = 1, 9, 9, 40, 24, 3, 3
     x = I.small_int(g, (N, H, W, Cin), code, -2, 2)
     w = I.small_int(g, (KH, KW, Cin, Cout), code, -2, 2)
     ref = oracle.conv2d(x, w, code, (1, 1), (1, 1), (1, 1), with_mag=False)
-    for split in (2, 3):
+    firsts = {}
+    for k in conv:
+        firsts.setdefault(k.family, k)
+    for k, split in ((k, s) for k in firsts.values() for s in (2, 3)):
         assert vx.vx_force_plan(k.id, split) == 0
         try:
             y1 = run_conv(x, w, code, (1, 1), (1, 1), (1, 1))
