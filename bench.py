@@ -78,18 +78,22 @@ def _profiled_traffic(kernel_name):
     taken on the current kernel sources for this kernel; else None."""
     path = os.path.join(ROOT, "profiles", "sweep_f16_traffic.txt")
     try:
-        kv = {}
+        kv, traffic = {}, {}
         with open(path) as f:
             for ln in f:
                 if ln.strip() and not ln.startswith("#"):
                     k, _, v = ln.strip().partition(" ")
-                    kv[k] = v
+                    if k == "traffic":
+                        name, _, b = v.partition(" ")
+                        traffic[name] = float(b)
+                    else:
+                        kv[k] = v
     except OSError:
         return None
     from paper_2409_01075_amd import vx
-    if kv.get("kernel") != kernel_name or kv.get("registry_hash") != vx.vx_registry_hash():
+    if kv.get("registry_hash") != vx.vx_registry_hash():
         return None
-    return float(kv["traffic_bytes_per_launch"])
+    return traffic.get(kernel_name)
 
 
 def _selector_kind():
