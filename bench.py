@@ -43,9 +43,13 @@ def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--workload", default="sweep",
-                    choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single", "mixed", "conv"],
-                    help="sweep (default, the headline metric), one of the other GEMM sets, or the "
-                         "dynamic-shape convolution set")
+                    choices=["sweep", "sweep-sample", "encoder", "attention", "llm", "single", "mixed", "conv", "shapes"],
+                    help="sweep (default, the headline metric), one of the other GEMM sets, the "
+                         "dynamic-shape convolution set, or the GEMMs listed by --shapes")
+    ap.add_argument("--shapes", default="",
+                    help="for --workload shapes: 'M,N,K[,batch];...' (operands N(0,1) and N(0,0.02))")
+    ap.add_argument("--dtype", default="bf16", choices=["f32", "f16", "bf16"],
+                    help="element type for --workload shapes")
     ap.add_argument("--trials", type=int, default=None, help="trials of a GEMM set (default: the full set)")
     ap.add_argument("--adapt", action="store_true",
                     help="hardware-adaptation study (Section 7.4): fp16, N in {1024, 2048, 4096}, K = 1024, "
@@ -96,6 +100,22 @@ def _profiled_traffic(kernel_name):
     return traffic.get(kernel_name)
 
 
+def _copy_calibration(args, dev):
+    """One plain device-to-device copy of --copy-mib MiB (a kernel of known
+    traffic for scaling memory counters taken under a profiler)."""
+    if args.copy_mib <= 0:
+        return
+    import torch
+    n = args.copy_mib * 2 ** 20 // 2
+    src = torch.empty(n, dtype=torch.float16, device=dev)
+    dst = torch.empty(n, dtype=torch.float16, device=dev)
+    src.fill_(1.0)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def _selector_kind():
     from paper_2409_01075_amd import vx
     return "hybrid (calibrated)" if vx.vx_calibration_active() else "analytical"
@@ -134,13 +154,28 @@ def _cpu_baseline(ms, budget_s):
                       % ("{%d..%d}" % (done[0], done[-1]), len(done))}
 
 
-def _set_jobs(name, trials):
+def _set_jobs(name, trials, shapes="", dtype="bf16"):
     """(label, batch, M, N, K, dtype, make) for every GEMM of a set; make(dev)
     returns seeded device operands (A, B) of the set's distributions."""
     from paper_2409_01075_amd import inputs as I
     import torch
     bf = torch.bfloat16
     jobs = []
+    if name == "shapes":
+        code = I.DTYPES[dtype]
+        tdt = {0: torch.float32, 1: torch.float16, 2: torch.bfloat16}[code]
+        for i, spec in enumerate(x for x in shapes.split(";") if x.strip()):
+            v = [int(t) for t in spec.split(",")]
+            if len(v) not in (3, 4) or min(v) < 1:
+                raise SystemExit("--shapes: 'M,N,K[,batch];...' with positive sizes")
+            M, N, K = v[:3]
+            b = v[3] if len(v) == 4 else 1
+            def mk(dev, i=i, b=b, M=M, N=N, K=K):
+                return (I.device_normal((b * M, K), 1.0, 1000 * i, dev, tdt),
+                        I.device_normal((b * K, N), 0.02, 1000 * i + 1, dev, tdt))
+            jobs.append(("%s (%d,%d)x(%d,%d)%s" % (dtype, M, K, K, N, " x%d" % b if b > 1 else ""), b, M, N, K,
+                         code, mk))
+        return jobs
     if name == "mixed":
         # the study's whole benchmark: samples of every set, so that a static
         # strategy has to serve the full range of shapes at once
@@ -581,7 +616,7 @@ def run_set(args):
     L = vx.lib()
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
-    jobs = _set_jobs(args.workload, args.trials)
+    jobs = _set_jobs(args.workload, args.trials, args.shapes, args.dtype)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     torch.cuda._sleep(1000000)
@@ -626,7 +661,8 @@ def run_set(args):
         bytes_min = float(set_bytes)
         t_mfma = flops / (MFMA_PEAK_TFLOPS[dt] * 1e12)
         t_hbm = bytes_min / (HBM_PEAK_GBPS * 1e9)
-        r = {"label": label, "batch": b, "M": M, "N": N, "K": K, "us": t * 1e6, "tflops": flops / t / 1e12,
+        r = {"label": label, "batch": b, "M": M, "N": N, "K": K, "dt": dt, "eb": eb, "us": t * 1e6,
+             "tflops": flops / t / 1e12,
              "gbps": bytes_min / t / 1e9, "bound": "mfma" if t_mfma >= t_hbm else "hbm",
              "roof_frac": max(t_mfma, t_hbm) / t, "kernel": plan.kernel_id, "split": plan.split_k,
              "tile": [plan.kernel.mb, plan.kernel.nb, plan.kernel.kb, plan.kernel.stages]}
@@ -662,19 +698,20 @@ def run_set(args):
     dom_bound = max(set(r["bound"] for r in dom), key=lambda x: sum(r["us"] for r in dom if r["bound"] == x))
     dom_t = sum(r["us"] for r in dom) * 1e-6
     if dom_bound == "hbm":
-        ach = sum(r["batch"] * (r["M"] * r["K"] + r["K"] * r["N"] + r["M"] * r["N"]) * 2.0 for r in dom) / dom_t / 1e9
+        ach = sum(r["batch"] * (r["M"] * r["K"] + r["K"] * r["N"] + r["M"] * r["N"]) * r["eb"] for r in dom) / dom_t / 1e9
         roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBPS}
     else:
         ach = sum(2.0 * r["batch"] * r["M"] * r["N"] * r["K"] for r in dom) / dom_t / 1e12
-        roof = {"bound": "mfma", "achieved": ach, "peak": MFMA_PEAK_TFLOPS[2], "unit": "TFLOP/s",
-                "frac": ach / MFMA_PEAK_TFLOPS[2]}
+        peak = MFMA_PEAK_TFLOPS[dom[0]["dt"]]
+        roof = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak}
     roof.update({"traffic": None, "kernel": "vxk_%d" % kid, "launches": len(dom),
                  "avg_us": dom_t / len(dom) * 1e6})
     out = {"metric": "GEMM TFLOP/s geomean over dynamic-M sweep; % of MFMA/HBM roofline on 1 GPU",
            "value": geo([r["tflops"] for r in results]), "unit": "TFLOP/s", "n_gpus": 1,
            "steps": 1, "warmup": 1, "ms_per_step": sum(r["us"] for r in results) / 1e3,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-           "dtype": "f32" if args.workload == "single" else "bf16", "data": "synthetic (seeded, on device)",
+           "dtype": ("f32" if args.workload == "single" else args.dtype if args.workload == "shapes" else "bf16"),
+           "data": "synthetic (seeded, on device)",
            "config": {"workload": args.workload, "gemms": len(results)},
            "roofline": roof,
            "roof_frac_geomean": geo([r["roof_frac"] for r in results]),
@@ -684,6 +721,7 @@ def run_set(args):
                           "frac_geomean": geo([r["roof_frac"] for r in mf])}}
     if args.compare_torch:
         out["vs_torch_matmul_geomean"] = geo([r["torch_us"] / r["us"] for r in results])
+    _copy_calibration(args, dev)
     if args.detail:
         with open(args.detail, "w") as f:
             json.dump(results, f)
@@ -817,15 +855,7 @@ def main():
         torch.cuda.synchronize()
         pass_ms.append(e0.elapsed_time(e1))
 
-    if args.copy_mib > 0:
-        n = args.copy_mib * 2 ** 20 // 2
-        src = torch.empty(n, dtype=torch.float16, device=dev)
-        dst = torch.empty(n, dtype=torch.float16, device=dev)
-        src.fill_(1.0)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    _copy_calibration(args, dev)
 
     med = np.median(np.array(per_step), axis=0)        # ms per call, per M
     flops = np.array([2.0 * M * N * K for M in ms])
