@@ -306,7 +306,7 @@ def run_study(args):
     e1.record(stream)
     torch.cuda.synchronize()
     spin = int(1e6 / max(e0.elapsed_time(e1), 1e-3) * 0.3)
-    reg = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count())) if k.op == 0]
+    reg = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]   # indexed by kernel id
     jobs = _set_jobs(args.workload, args.trials)
     rows, tables = [], []
     vx.vx_force_plan(-1, 0)
@@ -322,7 +322,7 @@ def run_study(args):
         t_pick = _time_calls(call, R, stream, spin)
         table = {}
         for k in reg:
-            if k.dtype != dt or not k.enabled or (k.vec and not vec_ok):
+            if k.op != 0 or k.dtype != dt or not k.enabled or (k.vec and not vec_ok):
                 continue
             for split in (1, 2, 4, 8):
                 st, _ = vx.vx_plan_cost(b, M, N, K, dt, k.id, split, vec_ok)
