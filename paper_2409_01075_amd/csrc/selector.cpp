@@ -127,6 +127,33 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     const int64_t active = std::min(units, slots);
     const double per_cu = (double)cdiv(active, hw.num_cu);
 
+    const double bytes_min = (double)sh.batch * ((double)sh.M * sh.K + (double)sh.K * sh.N + (double)sh.M * sh.N) * eb;
+    const double floor_ns = bytes_min / hw.hbm_gbps;
+    const double bw_wg = hw.l2_bytes_clk_cu * hw.clock_ghz / per_cu;                // B/ns, L2 -> one workgroup
+    // split-K epilogue: the partial tile out, the arrival counter, and the
+    // last arrival's reads of the other slices
+    const double part = (double)k.mb * k.nb * 4.0 / bw_wg;
+    const double t_split_model =
+        split > 1 ? part + hw.atomic_latency_ns + hw.mem_latency_ns + (double)(split - 1) * part : 0.0;
+
+    const VxCalib* cb = vxi_calib(k.id);
+    if (cb) {
+        // empirical low levels, analytical grid level
+        double t_split = t_split_model;                                     // split-K epilogue, analytical
+        if (split > 1 && cb->split_a >= 0.0 && cb->split_b >= 0.0)
+            t_split = cb->split_a + cb->split_b * (double)(split - 1);      // ... or measured
+        const double load_last = (double)(units - (F - 1) * slots) / (double)slots;
+        auto at_load = [&](double full, double light) {
+            if (load_last <= cb->load_light || cb->load_light >= 1.0)
+                return light;
+            return light + (full - light) * (load_last - cb->load_light) / (1.0 - cb->load_light);
+        };
+        const double wave_full = cb->fix_full + (double)nk * cb->step_full;
+        const double wave_last = at_load(cb->fix_full, cb->fix_light) + (double)nk * at_load(cb->step_full, cb->step_light);
+        const double cost2 = (double)(F - 1) * wave_full + wave_last + t_split;
+        return vxi_calib_launch_ns(hw) + std::max(cost2, floor_ns);
+    }
+
     // Level 0: one K step of MFMAs fed from LDS (Eq. 2 over the Kb/k0 sub-steps),
     // or of vector-ALU dot products on B chunks held in registers (family 2:
     // v_dot2 retires 4 FLOP per lane, v_fma 2, one wave instruction per SIMD
@@ -145,7 +172,6 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     const double cost0 = vx_cost_temporal(t_lds, sub, c_mfma, 0.0);
 
     // Level 1: the K loop of one workgroup (Eq. 2 over n_k K steps).
-    const double bw_wg = hw.l2_bytes_clk_cu * hw.clock_ghz / per_cu;                // B/ns
     // element-aligned operands: the same 16-byte loads, but misaligned ones
     // straddle an extra cache line per row segment and the ragged edge chunks
     // are gathered element by element
@@ -153,11 +179,7 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     // (family 2 reads only B from memory in the loop; its A slice is loaded once)
     const double xfer = (double)(valu ? k.nb : k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
     const double t_load = hw.mem_latency_ns + xfer;
-    double t_store = (double)k.mb * k.nb * eb / bw_wg;
-    if (split > 1) {
-        const double part = (double)k.mb * k.nb * 4.0 / bw_wg;
-        t_store += part + hw.atomic_latency_ns + hw.mem_latency_ns + (double)(split - 1) * part;
-    }
+    const double t_store = (double)k.mb * k.nb * eb / bw_wg + t_split_model;
     const int depth = valu ? 1 : std::max(1, k.stages - 1);   // family 2: two register sets
     double t1;
     if (depth == 1 || nk <= 1) {
@@ -165,27 +187,6 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     } else {
         const double t_issue = std::max(xfer, t_load / depth);
         t1 = t_load + (double)(nk - 1) * std::max(t_issue, cost0) + cost0 + t_store;
-    }
-
-    const double bytes_min = (double)sh.batch * ((double)sh.M * sh.K + (double)sh.K * sh.N + (double)sh.M * sh.N) * eb;
-    const double floor_ns = bytes_min / hw.hbm_gbps;
-
-    const VxCalib* cb = vxi_calib(k.id);
-    if (cb) {
-        // empirical low levels, analytical grid level
-        double t_split = t_store - (double)k.mb * k.nb * eb / bw_wg;   // split-K epilogue, analytical
-        if (split > 1 && cb->split_a >= 0.0 && cb->split_b >= 0.0)
-            t_split = cb->split_a + cb->split_b * (double)(split - 1);      // ... or measured
-        const double load_last = (double)(units - (F - 1) * slots) / (double)slots;
-        auto at_load = [&](double full, double light) {
-            if (load_last <= cb->load_light || cb->load_light >= 1.0)
-                return light;
-            return light + (full - light) * (load_last - cb->load_light) / (1.0 - cb->load_light);
-        };
-        const double wave_full = cb->fix_full + (double)nk * cb->step_full;
-        const double wave_last = at_load(cb->fix_full, cb->fix_light) + (double)nk * at_load(cb->step_full, cb->step_light);
-        const double cost2 = (double)(F - 1) * wave_full + wave_last + t_split;
-        return vxi_calib_launch_ns(hw) + std::max(cost2, floor_ns);
     }
 
     // Level 2 (Eq. 4), dispatch constant, compulsory-traffic floor.
@@ -214,6 +215,8 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
             continue;
         if (!(f.backends & (k.family == 2 ? 2 : 1)))
             continue;
+        if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || k.op != sh.op)
+            continue;   // infeasible at every split (the same test opens vxi_cost)
         for (int s : kSplits) {
             int split = s;
             if (forced_split > 0) {
