@@ -231,6 +231,30 @@ def generate_candidates_for_layer(level, dtype, hw=GFX950, family=None):
 REG_FALLBACK_16 = [(32, 32, 128, 2, 2, 16), (64, 64, 64, 2, 2, 16), (128, 128, 64, 2, 2, 32)]
 
 
+# Wide tiles (direct-to-LDS, fp16/bf16): workgroup tiles with a 192 side --
+# an integer multiple (3) of the 64-wide step between the power-of-two tiles,
+# outside the power-of-two L1 set above -- with 8 wavefronts whose tiles
+# follow the L1 rules (accumulators, aspect <= 4).  They give the grid level
+# tile counts between those of the 128 and 256 tiles: a 6976 x 768 output is
+# 330 tiles of 128 x 128 (1.3 per CU) but 222 of 192 x 128.
+WIDE_TILES = [(192, 128), (128, 192), (192, 192), (256, 192), (192, 256)]
+
+
+def dma_wide_candidates(dtype, hw=GFX950):
+    out = []
+    for (mb, nb) in WIDE_TILES:
+        for (wm, wn) in ((2, 4), (4, 2)):
+            mw, nw = mb // wm, nb // wn
+            acc = mw * nw // hw["wave"]
+            if mw % 16 or nw % 16 or not (4 <= acc <= 256) or max(mw, nw) > 4 * min(mw, nw):
+                continue
+            mi = 32 if (mw % 32 == 0 and nw % 32 == 0 and min(mw, nw) >= 64) else 16
+            c = (mb, nb, 64, wm, wn, mi)
+            for st in dma_stage_options(*c, 1, hw):
+                out.append(_entry(dtype, "dma", st, c, 1, hw))
+    return out
+
+
 def _entry(dtype, family, stages, c, vec, hw):
     mb, nb, kb, wm, wn, mi = c
     lds = lds_bytes_dma(mb, nb, kb, stages) if family == "dma" else lds_bytes(dtype, mb, nb, kb)
@@ -350,6 +374,8 @@ def registry(hw=GFX950):
         out += conv_candidates(dtype, hw)
     for dtype in ("f16", "bf16"):
         out += conv_dma_candidates(dtype, hw)
+    for dtype in ("f16", "bf16"):
+        out += dma_wide_candidates(dtype, hw)
     for i, e in enumerate(out):
         e["id"] = i
     return out

@@ -12,7 +12,8 @@
 //
 // LDS layouts (dense, 16-byte chunks XOR-swizzled against bank conflicts):
 //   As[m][k]  Mb x Kb, k contiguous   (chunk c of row m stored at c ^ swzA(m))
-//   Bs[k][n]  Kb x Nb, n contiguous   (chunk c of row k stored at c ^ swzB(k))
+//   Bs[k][n]  Kb x Nb, n contiguous   (chunk c of row k stored at c ^ swzB(k);
+//                                     rotated by swzB(k) in rows of 24 chunks)
 // B stays in its natural n-contiguous layout; the MFMA fragments of B are
 // read with the transposing LDS read: in each 16-lane group, source lane s
 // points at Bs[k0 + s/4][n0 + 4*(s%4)], and output lane j receives
@@ -69,8 +70,28 @@ struct DCfg {
 };
 
 __device__ __forceinline__ int swz_a(int r, int period) { return r & (period - 1); }
+// B rows hold CPB 16-byte chunks.  With CPB a power of two, logical chunk c
+// of row k sits at position c ^ s(k), s(k) = 2 (k mod 4) mod CPB (an XOR is
+// its own inverse).  Rows of 24 chunks (tiles 192 wide) rotate instead:
+// chunk c at position (c + s(k)) mod CPB.
 template <int CPB>
-__device__ __forceinline__ int swz_b(int k) { return (2 * (k & 3)) & (CPB - 1); }
+__device__ __forceinline__ int swz_b(int k) { return (CPB & (CPB - 1)) == 0 ? (2 * (k & 3)) & (CPB - 1) : (2 * (k & 3)) % CPB; }
+template <int CPB>
+__device__ __forceinline__ int b_pos(int c, int k)   // LDS position of logical chunk c of row k
+{
+    if constexpr ((CPB & (CPB - 1)) == 0)
+        return c ^ swz_b<CPB>(k);
+    else
+        return (c + swz_b<CPB>(k)) % CPB;
+}
+template <int CPB>
+__device__ __forceinline__ int b_chunk(int pos, int k)   // logical chunk held at LDS position pos of row k
+{
+    if constexpr ((CPB & (CPB - 1)) == 0)
+        return pos ^ swz_b<CPB>(k);
+    else
+        return (pos + CPB - swz_b<CPB>(k)) % CPB;
+}
 
 // s_waitcnt vmcnt(n) for a compile-time n (expcnt and lgkmcnt left at max).
 template <int N>
@@ -239,7 +260,7 @@ struct DmaTile {
             // B: rows k0.. of the batch's B, columns from n0
             const int instr = wave * C::B_IPW + (I - C::A_IPW);
             const int slot = instr * 64 + lane;
-            const int k = slot / C::CPB, c = (slot % C::CPB) ^ swz_b<C::CPB>(k);
+            const int k = slot / C::CPB, c = b_chunk<C::CPB>(slot % C::CPB, k);
             const bool ok = k < kv && c * 8 < nv;
             dma_lds<C::LANE_BYTES>(rb, stage + C::A_BYTES + instr * C::WAVE_BYTES,
                                    ok ? (unsigned)((k * N + c * 8) * 2) : kOOB);
@@ -286,8 +307,8 @@ __device__ __forceinline__ void dma_frags(lds_char* stage, u32x4 (&fa)[C::FM], u
     for (int fn = 0; fn < C::FN; ++fn) {
         const int n = wn0 + fn * C::MI + tr_n;
         const int k1 = kk * C::KI + tr_k, k2 = k1 + 4;
-        lds_char* p1 = Bs + k1 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k1)) << 4) + (n & 7) * 2;
-        lds_char* p2 = Bs + k2 * (C::NB * 2) + (((n >> 3) ^ swz_b<C::CPB>(k2)) << 4) + (n & 7) * 2;
+        lds_char* p1 = Bs + k1 * (C::NB * 2) + (b_pos<C::CPB>(n >> 3, k1) << 4) + (n & 7) * 2;
+        lds_char* p2 = Bs + k2 * (C::NB * 2) + (b_pos<C::CPB>(n >> 3, k2) << 4) + (n & 7) * 2;
         const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p1);
         const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p2);
         const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
