@@ -58,6 +58,8 @@ def _parse():
                     help="selector quality study: time every feasible (kernel, split) plan of each GEMM "
                          "of the set and compare the selector's pick, and the Static1/Static2 hierarchy "
                          "ablations, with the best")
+    ap.add_argument("--no-hybrid", action="store_true",
+                    help="ablation: the selector does not consider the hybrid grid")
     ap.add_argument("--no-calibration", action="store_true",
                     help="ablation: plan with the purely analytical cost model (ignore the calibration table)")
     ap.add_argument("--compare-torch", action="store_true",
@@ -266,6 +268,12 @@ def _study_ctx(job, dev, rot_mib, L, sp):
     return call, R, (pa, pb, pc)
 
 
+def _plan_key(plan):
+    """(kernel, split) of a plan; the split is negative for a hybrid grid (the
+    form vx_force_plan and vx_plan_cost take)."""
+    return (plan.kernel_id, -plan.split_k if plan.dp_tiles else plan.split_k)
+
+
 def _wave(k):
     return (k.mb // k.wm, k.nb // k.wn, k.mfma_m)
 
@@ -283,7 +291,8 @@ def run_study(args):
     """Selector quality and the hierarchy ablations (Section 7.4).
 
     Pass 1, per GEMM of the set: the time of the selector's plan and of every
-    feasible (kernel, split in {1, 2, 4, 8}) plan of the registry; the best of
+    feasible (kernel, split in {1, 2, 4, 8}, plain grid or hybrid grid for
+    splits 2 and 4) plan of the registry; the best of
     them stands in for the per-shape profiled upper bound.
     Pass 2, per dtype and alignment class of the set: Static1 fixes the
     wavefront strategy (wavefront tile and MFMA instruction) that is most
@@ -324,7 +333,7 @@ def run_study(args):
         for k in reg:
             if k.op != 0 or k.dtype != dt or not k.enabled or (k.vec and not vec_ok):
                 continue
-            for split in (1, 2, 4, 8):
+            for split in (1, 2, 4, 8, -2, -4):   # negative: the hybrid grid
                 st, _ = vx.vx_plan_cost(b, M, N, K, dt, k.id, split, vec_ok)
                 if st != 0:
                     continue
@@ -335,7 +344,7 @@ def run_study(args):
                 finally:
                     vx.vx_force_plan(-1, 0)
         del keep, call
-        pick = (plan.kernel_id, plan.split_k)
+        pick = _plan_key(plan)
         table[pick] = min(t_pick, table.get(pick, t_pick))
         bk = min(table, key=table.get)
         kb = reg[bk[0]]
@@ -363,7 +372,7 @@ def run_study(args):
         fixed[c] = (s1, _most_frequent(per) if per else None)
 
     def timed_plan(i, plan):
-        key = (plan.kernel_id, plan.split_k)
+        key = _plan_key(plan)
         if key not in tables[i]:
             call, R, keep = _study_ctx(jobs[i], dev, args.rot_mib, L, sp)
             vx.vx_force_plan(*key)
@@ -738,6 +747,9 @@ def main():
     if args.no_calibration:
         from paper_2409_01075_amd import vx
         vx.vx_calibration_enable(0)
+    if args.no_hybrid:
+        from paper_2409_01075_amd import vx
+        vx.vx_enable_hybrid_grid(0)
     if args.study:
         run_study(args)
         return

@@ -111,6 +111,9 @@ typedef struct vx_plan {
                                       4-column chunks of C are stored as one vector either way) */
     int64_t tiles_m, tiles_n;
     int64_t grid;                  /* workgroups launched */
+    int64_t dp_tiles;              /* hybrid grid (> 0): this many output tiles, whole waves of the
+                                      device, run whole, one workgroup each, and only the others
+                                      are split split_k ways; 0: every tile is split split_k ways */
     int group_m;
     size_t workspace_bytes;        /* fp32 partials needed by split_k > 1 */
     double predicted_ns;           /* the cost model's estimate for the call */
@@ -147,6 +150,7 @@ vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype
 /*
  * The cost model's estimate (ns) for running a given kernel with a given
  * split-K factor on a shape; VX_ERR_NO_CANDIDATE if the pair is infeasible.
+ * split_k < 0 prices the hybrid grid with -split_k slices per split tile.
  */
 vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype,
                        int kernel_id, int split_k, int vec_ok, double* out_ns);
@@ -194,8 +198,10 @@ vx_status vx_kernel_occupancy(int kernel_id, int* wgs_per_cu);
 
 /*
  * Pin every following call to one kernel and split-K factor (kernel_id < 0
- * restores the analytical choice; split_k <= 0 lets the selector pick the
- * split for the forced kernel).  For tests and ablation studies; process-wide.
+ * restores the analytical choice; split_k == 0 lets the selector pick the
+ * split and grid for the forced kernel; split_k < 0 forces the hybrid grid
+ * with -split_k slices per split tile, VX_ERR_NO_CANDIDATE at calls whose
+ * tiles do not exceed one wave of the device).  For tests and ablation studies; process-wide.
  * A forced kernel of the wrong dtype or alignment class makes calls return
  * VX_ERR_NO_CANDIDATE.
  */
@@ -225,6 +231,14 @@ vx_status vx_fix_wavefront(int wave_m, int wave_n, int mfma_m);
  * Process-wide; for studies and tests.
  */
 vx_status vx_restrict_backends(int mask);
+
+/*
+ * Grid-level ablation: with enable = 0 the selector no longer considers the
+ * hybrid grid (whole waves of whole tiles plus the remaining tiles split K
+ * ways, see vx_plan.dp_tiles); 1 (the default) restores it.  Forced plans
+ * (vx_force_plan) are not affected.  Process-wide; for studies and tests.
+ */
+vx_status vx_enable_hybrid_grid(int enable);
 
 /*
  * Hand the library a caller-owned device buffer to use as the split-K

@@ -36,6 +36,7 @@ std::atomic<int> g_force_id{-1};
 std::atomic<int> g_force_split{0};
 std::atomic<int> g_fix_wm{0}, g_fix_wn{0}, g_fix_mi{0};
 std::atomic<int> g_backends{3};   // kernel backends the selector may use (vx_restrict_backends)
+std::atomic<bool> g_hybrid{true};  // hybrid grids among the plans (vx_enable_hybrid_grid)
 std::atomic<uint64_t> g_epoch{0};   // bumps when planning inputs change
 
 struct PlanKey {
@@ -216,6 +217,7 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
     f.wave_n = g_fix_wn.load();
     f.mfma_m = g_fix_mi.load();
     f.backends = g_backends.load();
+    f.hybrid = g_hybrid.load();
     vx_hwinfo hw;
     vx_status st = hwinfo_for(dev, &hw);
     if (st != VX_OK)
@@ -370,6 +372,7 @@ vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream)
     a.group_m = plan.group_m;
     a.num_xcd = hw.num_xcd;
     a.grid = (int)plan.grid;
+    a.dp_tiles = (int)plan.dp_tiles;
     a.ws = plan.split_k > 1 ? (float*)(ws.base + kTicketBytes) : nullptr;
     a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
     hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);
@@ -674,7 +677,7 @@ vx_status vx_force_plan(int kernel_id, int split_k)
     if (kernel_id >= vx_registry_count())
         return VX_ERR_NO_CANDIDATE;
     g_force_id.store(kernel_id < 0 ? -1 : kernel_id);
-    g_force_split.store(split_k > 0 ? split_k : 0);
+    g_force_split.store(kernel_id < 0 ? 0 : split_k);
     return VX_OK;
 }
 
@@ -693,6 +696,15 @@ vx_status vx_restrict_backends(int mask)
         return VX_ERR_NO_CANDIDATE;
     std::lock_guard<std::mutex> lk(g_mu);
     g_backends.store(mask);
+    g_plans.clear();
+    g_epoch.fetch_add(1);
+    return VX_OK;
+}
+
+vx_status vx_enable_hybrid_grid(int enable)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_hybrid.store(enable != 0);
     g_plans.clear();
     g_epoch.fetch_add(1);
     return VX_OK;

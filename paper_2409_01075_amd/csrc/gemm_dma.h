@@ -440,7 +440,7 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
     }
     wait_vm<0>();   // nothing is in flight here; kept as a guard before LDS is released
 #undef VX_STAGE
-    if (p.split > 1 && !reduce_split<C>(p, acc, g, t))
+    if (g.split > 1 && !reduce_split<C>(p, acc, g, t))
         return;
     if constexpr (C::LDS_EPI) {
         __syncthreads();   // every wave has finished reading the ring

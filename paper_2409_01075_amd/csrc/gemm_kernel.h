@@ -475,7 +475,8 @@ __device__ __forceinline__ VxGemmArgs pin_args(const VxGemmArgs& in)
     VxGemmArgs p = in;
     asm volatile("" : "+s"(p.A), "+s"(p.B), "+s"(p.C), "+s"(p.sA), "+s"(p.sB), "+s"(p.sC), "+s"(p.M), "+s"(p.N),
                       "+s"(p.K), "+s"(p.tiles_m), "+s"(p.tiles_n), "+s"(p.split), "+s"(p.k_per_split),
-                      "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.ws), "+s"(p.tickets));
+                      "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.dp_tiles), "+s"(p.ws),
+                      "+s"(p.tickets));
     return p;
 }
 
@@ -488,8 +489,11 @@ __device__ __forceinline__ void pin_conv(VxGemmArgs& p)
 
 // ---------------------------------------------------------- level 2 -------
 // Grid level: the parallel loop over (batch, K slice, tile) of one launch.
+// split is the number of K slices of this workgroup's tile (1 for a whole
+// tile of a hybrid grid) and rid the tile's index among the split tiles (its
+// slot in the split-K workspace and arrival counters).
 struct GridPos {
-    int b, z, tm, tn, m0, n0, kbeg, kend, nk, tiles;
+    int b, z, tm, tn, m0, n0, kbeg, kend, nk, tiles, split, rid;
 };
 
 template <int MB, int NB, int KB>
@@ -498,17 +502,37 @@ __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
     // Workgroups are dispatched round-robin over the XCDs; remap the linear id
     // so that each XCD receives a contiguous range of logical tiles
     // (neighbouring tiles share A or B panels in that XCD's L2).
-    const int G = p.grid, w = blockIdx.x;
+    // A hybrid grid remaps its two classes of workgroups -- the whole tiles
+    // [0, dp_tiles), dispatched first, and the split tiles' slices after them
+    // -- each on its own; dp_tiles is a multiple of num_xcd, so a workgroup's
+    // XCD is its index within the class modulo num_xcd as well.
+    const int w = blockIdx.x;
     const int nx = p.num_xcd;
-    const int xcd = w % nx, q = G / nx, rem = G % nx;
-    const int wl = xcd * q + (xcd < rem ? xcd : rem) + w / nx;
+    const bool hyb = p.dp_tiles > 0;
+    const bool whole = hyb && w < p.dp_tiles;
+    const int wc = hyb && !whole ? w - p.dp_tiles : w;
+    const int G = hyb ? (whole ? p.dp_tiles : p.grid - p.dp_tiles) : p.grid;
+    const int xcd = wc % nx, q = G / nx, rem = G % nx;
+    const int wl = xcd * q + (xcd < rem ? xcd : rem) + wc / nx;
 
     GridPos g;
     g.tiles = p.tiles_m * p.tiles_n;
-    const int tile = wl % g.tiles;
-    const int bz = wl / g.tiles;
-    g.z = bz % p.split;
-    g.b = bz / p.split;
+    int tile;
+    if (!hyb) {
+        tile = wl % g.tiles;
+        const int bz = wl / g.tiles;
+        g.z = bz % p.split;
+        g.b = bz / p.split;
+        g.split = p.split;
+    } else {
+        const int rt = p.batch * g.tiles - p.dp_tiles;   // tiles that are split
+        const int T = whole ? wl : p.dp_tiles + wl % rt;
+        g.z = whole ? 0 : wl / rt;
+        g.b = T / g.tiles;
+        tile = T % g.tiles;
+        g.split = whole ? 1 : p.split;
+        g.rid = whole ? 0 : wl % rt;
+    }
     // grouped order: group_m tile rows are walked column by column
     const int per_group = p.group_m * p.tiles_n;
     const int grp = tile / per_group;
@@ -518,8 +542,10 @@ __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
     g.tn = (tile % per_group) / gm;
     g.m0 = g.tm * MB;
     g.n0 = g.tn * NB;
-    g.kbeg = g.z * p.k_per_split;
-    g.kend = min(p.K, g.kbeg + p.k_per_split);
+    if (!hyb)
+        g.rid = g.b * g.tiles + g.tm * p.tiles_n + g.tn;
+    g.kbeg = whole ? 0 : g.z * p.k_per_split;
+    g.kend = whole ? p.K : min(p.K, g.kbeg + p.k_per_split);
     g.nk = g.kend > g.kbeg ? (g.kend - g.kbeg + KB - 1) / KB : 0;
     return g;
 }
@@ -550,9 +576,9 @@ template <int V>
 __device__ __forceinline__ bool split_reduce(const VxGemmArgs& p, const GridPos& g, f32x4 (&v)[V], int t, int nact)
 {
     const unsigned SLICE_BYTES = (unsigned)V * (unsigned)nact * 16u;
-    const int64_t tile_id = (int64_t)g.b * g.tiles + g.tm * p.tiles_n + g.tn;
+    const int64_t tile_id = g.rid;
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.ws + tile_id * (int64_t)p.split * (V * nact * 4)), (short)0, (int)(SLICE_BYTES * p.split), 0x00020000);
+        (void*)(p.ws + tile_id * (int64_t)g.split * (V * nact * 4)), (short)0, (int)(SLICE_BYTES * g.split), 0x00020000);
     constexpr int SC1 = 16;   // cache policy: device scope
     const bool act = t < nact;
     const unsigned mine = (unsigned)g.z * SLICE_BYTES;
@@ -569,7 +595,7 @@ __device__ __forceinline__ bool split_reduce(const VxGemmArgs& p, const GridPos&
     if (t == 0)
         arrived = __hip_atomic_fetch_add(&p.tickets[tile_id], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    if (arrived != (unsigned)(p.split - 1))
+    if (arrived != (unsigned)(g.split - 1))
         return false;
     // Sum slices 0..split-1 in order.  The loads of SF slices are issued
     // together before any of them is added, so the reduction waits for one
@@ -578,11 +604,11 @@ __device__ __forceinline__ bool split_reduce(const VxGemmArgs& p, const GridPos&
     if (act) {
         constexpr int SF = V <= 2 ? 8 : V <= 4 ? 4 : V <= 8 ? 2 : 1;
         f32x4 sum[V];
-        for (int zz0 = 0; zz0 < p.split; zz0 += SF) {
+        for (int zz0 = 0; zz0 < g.split; zz0 += SF) {
             f32x4 part[SF][V];
 #pragma unroll
             for (int j = 0; j < SF; ++j) {
-                const int zz = min(zz0 + j, p.split - 1);   // in range; surplus loads are not added
+                const int zz = min(zz0 + j, g.split - 1);   // in range; surplus loads are not added
 #pragma unroll
                 for (int e4 = 0; e4 < V; ++e4)
                     part[j][e4] = __builtin_bit_cast(
@@ -591,7 +617,7 @@ __device__ __forceinline__ bool split_reduce(const VxGemmArgs& p, const GridPos&
             }
 #pragma unroll
             for (int j = 0; j < SF; ++j) {
-                if (zz0 + j >= p.split)
+                if (zz0 + j >= g.split)
                     break;
 #pragma unroll
                 for (int e4 = 0; e4 < V; ++e4)
@@ -853,7 +879,7 @@ __device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
         __syncthreads();
     }
     // the loop ends with a barrier: LDS is idle here
-    if (p.split > 1 && !reduce_split<C>(p, acc, g, t))
+    if (g.split > 1 && !reduce_split<C>(p, acc, g, t))
         return;
     if constexpr (C::LDS_EPI)
         store_lds<C>(p, acc, g, t, lane, wm0, wn0, (lds_char*)smem);

@@ -211,7 +211,7 @@ __device__ __forceinline__ void gemm_valu_body(const VxGemmArgs& args)
         for (int w = 0; w < C::WAVES; ++w)
             out += *(__attribute__((address_space(3))) f32x4*)(red + (w * C::MT + m) * C::NB + nn);
     }
-    if (p.split > 1) {
+    if (g.split > 1) {
         f32x4 v[1] = {out};
         if (!split_reduce<1>(p, g, v, t, C::OUT4))
             return;

@@ -72,9 +72,17 @@ int vxi_occupancy(const vx_hwinfo& hw, const vx_kernel_info& k)
 }
 
 double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k, int split,
-                const VxLimits& lim, int* k_per_split)
+                const VxLimits& lim, int* k_per_split, int64_t* dp_tiles)
 {
+    // split < 0: the hybrid grid -- whole waves of whole tiles, and the
+    // remaining tiles split -split ways (the last, partial wave of the plain
+    // grid spread over more workgroups)
+    const bool hyb = split < 0;
+    if (hyb)
+        split = -split;
     if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || split < 1 || k.op != sh.op)
+        return -1.0;
+    if (hyb && (split < 2 || sh.K == 0))
         return -1.0;
     const int eb = sh.dt == VX_F32 ? 4 : 2;
     const int64_t tiles_m = cdiv(sh.M, k.mb), tiles_n = cdiv(sh.N, k.nb);
@@ -91,15 +99,23 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     }
     if (kps > INT32_MAX || tiles > INT32_MAX)
         return -1.0;
-    if (k.k_max > 0 && kps > k.k_max)   // the kernel holds a whole slice of A in LDS
+    if (k.k_max > 0 && (hyb ? sh.K : kps) > k.k_max)   // the kernel holds a whole slice of A in LDS
         return -1.0;
-    const int64_t units = tiles * split;
+
+    const int waves = k.wm * k.wn;
+    const int occ = vxi_occupancy(hw, k);
+    const int64_t slots = (int64_t)hw.num_cu * occ;
+    const int64_t dp = hyb ? tiles / slots * slots : 0;   // whole tiles, in whole waves
+    const int64_t split_tiles = tiles - dp;
+    if (hyb && (dp == 0 || split_tiles == 0 || slots % std::max(1, hw.num_xcd) != 0))
+        return -1.0;   // (the kernels remap each class of workgroups over the XCDs on its own)
+    const int64_t units = dp + split_tiles * split;
     if (units > INT32_MAX)
         return -1.0;
     if (split > 1) {
-        if (tiles > lim.max_tickets)
+        if (split_tiles > lim.max_tickets)
             return -1.0;
-        if ((double)tiles * split * k.mb * k.nb * 4.0 > (double)lim.ws_bytes)
+        if ((double)split_tiles * split * k.mb * k.nb * 4.0 > (double)lim.ws_bytes)
             return -1.0;
     }
     if (k.family == 1) {
@@ -112,37 +128,40 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     }
     if (k.family == 2) {
         // the vector-ALU kernels address a whole slice of B with 32-bit offsets
-        if ((double)kps * sh.N * eb >= 2147483648.0)
+        if ((double)(hyb ? sh.K : kps) * sh.N * eb >= 2147483648.0)
             return -1.0;
     }
     if (k_per_split)
         *k_per_split = (int)kps;
+    if (dp_tiles)
+        *dp_tiles = dp;
+    const int64_t nk_whole = cdiv(sh.K, k.kb);
 
-    const int waves = k.wm * k.wn;
-    const int occ = vxi_occupancy(hw, k);
-    const int64_t slots = (int64_t)hw.num_cu * occ;
-
-    // Level 2: wave quantisation over the device (Eq. 3).
-    const int64_t F = vx_cost_parallel_factor(units, slots);
-    const int64_t active = std::min(units, slots);
+    // Level 2: wave quantisation over the device (Eq. 3); a hybrid grid runs
+    // dp / slots full waves of whole tiles, then the split tiles' slices.
+    const int64_t units_s = hyb ? split_tiles * split : units;
+    const int64_t F = vx_cost_parallel_factor(units_s, slots);
+    const int64_t active = std::min(units_s, slots);
     const double per_cu = (double)cdiv(active, hw.num_cu);
+    const int64_t F_dp = dp / slots;
 
     const double bytes_min = (double)sh.batch * ((double)sh.M * sh.K + (double)sh.K * sh.N + (double)sh.M * sh.N) * eb;
     const double floor_ns = bytes_min / hw.hbm_gbps;
-    const double bw_wg = hw.l2_bytes_clk_cu * hw.clock_ghz / per_cu;                // B/ns, L2 -> one workgroup
+    auto bw_wg_at = [&](double pc) { return hw.l2_bytes_clk_cu * hw.clock_ghz / pc; };   // B/ns, L2 -> one workgroup
     // split-K epilogue: the partial tile out, the arrival counter, and the
     // last arrival's reads of the other slices
-    const double part = (double)k.mb * k.nb * 4.0 / bw_wg;
-    const double t_split_model =
-        split > 1 ? part + hw.atomic_latency_ns + hw.mem_latency_ns + (double)(split - 1) * part : 0.0;
+    auto t_split_at = [&](double pc) {
+        const double part = (double)k.mb * k.nb * 4.0 / bw_wg_at(pc);
+        return split > 1 ? part + hw.atomic_latency_ns + hw.mem_latency_ns + (double)(split - 1) * part : 0.0;
+    };
 
     const VxCalib* cb = vxi_calib(k.id);
     if (cb) {
         // empirical low levels, analytical grid level
-        double t_split = t_split_model;                                     // split-K epilogue, analytical
+        double t_split = t_split_at(per_cu);                                // split-K epilogue, analytical
         if (split > 1 && cb->split_a >= 0.0 && cb->split_b >= 0.0)
             t_split = cb->split_a + cb->split_b * (double)(split - 1);      // ... or measured
-        const double load_last = (double)(units - (F - 1) * slots) / (double)slots;
+        const double load_last = (double)(units_s - (F - 1) * slots) / (double)slots;
         auto at_load = [&](double full, double light) {
             if (load_last <= cb->load_light || cb->load_light >= 1.0)
                 return light;
@@ -150,47 +169,52 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
         };
         const double wave_full = cb->fix_full + (double)nk * cb->step_full;
         const double wave_last = at_load(cb->fix_full, cb->fix_light) + (double)nk * at_load(cb->step_full, cb->step_light);
-        const double cost2 = (double)(F - 1) * wave_full + wave_last + t_split;
+        const double wave_dp = cb->fix_full + (double)nk_whole * cb->step_full;
+        const double cost2 = (double)F_dp * wave_dp + (double)(F - 1) * wave_full + wave_last + t_split;
         return vxi_calib_launch_ns(hw) + std::max(cost2, floor_ns);
     }
 
-    // Level 0: one K step of MFMAs fed from LDS (Eq. 2 over the Kb/k0 sub-steps),
-    // or of vector-ALU dot products on B chunks held in registers (family 2:
-    // v_dot2 retires 4 FLOP per lane, v_fma 2, one wave instruction per SIMD
-    // every 4 clocks; A comes from LDS at a few bytes per k).
+    // Levels 0 and 1 for a workgroup of nk_ K steps and split_ slices, with
+    // pc workgroups sharing each CU.
     const bool valu = k.family == 2;
-    const double flop_clk = valu ? 64.0 * hw.simd_per_cu * (sh.dt == VX_F32 ? 0.5 : 1.0)
-                                 : (sh.dt == VX_F32 ? hw.mfma_flop_clk_cu_f32 : hw.mfma_flop_clk_cu_f16);
-    const double rate_wg = flop_clk * hw.clock_ghz *
-                           std::min((double)waves / hw.simd_per_cu, 1.0 / per_cu);   // FLOP/ns
-    const int kstep = valu ? k.kb : k.mfma_k * (sh.dt == VX_F32 ? 4 : 1);  // fp32 loads 4 MFMA steps at once
-    const int64_t sub = std::max<int64_t>(1, k.kb / kstep);
-    const double c_mfma = 2.0 * k.mb * k.nb * kstep / rate_wg;
-    const double lds_bw = hw.lds_bytes_clk_cu * hw.clock_ghz / per_cu;             // B/ns
-    const double t_lds = valu ? (double)k.threads * k.stages * k.mb * 4.0 / lds_bw
-                              : (double)waves * ((double)k.mb / k.wm + (double)k.nb / k.wn) * kstep * eb / lds_bw;
-    const double cost0 = vx_cost_temporal(t_lds, sub, c_mfma, 0.0);
+    auto t1_for = [&](int64_t nk_, bool split_epilogue, double pc) {
+        // Level 0: one K step of MFMAs fed from LDS (Eq. 2 over the Kb/k0 sub-steps),
+        // or of vector-ALU dot products on B chunks held in registers (family 2:
+        // v_dot2 retires 4 FLOP per lane, v_fma 2, one wave instruction per SIMD
+        // every 4 clocks; A comes from LDS at a few bytes per k).
+        const double flop_clk = valu ? 64.0 * hw.simd_per_cu * (sh.dt == VX_F32 ? 0.5 : 1.0)
+                                     : (sh.dt == VX_F32 ? hw.mfma_flop_clk_cu_f32 : hw.mfma_flop_clk_cu_f16);
+        const double rate_wg = flop_clk * hw.clock_ghz *
+                               std::min((double)waves / hw.simd_per_cu, 1.0 / pc);   // FLOP/ns
+        const int kstep = valu ? k.kb : k.mfma_k * (sh.dt == VX_F32 ? 4 : 1);  // fp32 loads 4 MFMA steps at once
+        const int64_t sub = std::max<int64_t>(1, k.kb / kstep);
+        const double c_mfma = 2.0 * k.mb * k.nb * kstep / rate_wg;
+        const double lds_bw = hw.lds_bytes_clk_cu * hw.clock_ghz / pc;             // B/ns
+        const double t_lds = valu ? (double)k.threads * k.stages * k.mb * 4.0 / lds_bw
+                                  : (double)waves * ((double)k.mb / k.wm + (double)k.nb / k.wn) * kstep * eb / lds_bw;
+        const double cost0 = vx_cost_temporal(t_lds, sub, c_mfma, 0.0);
 
-    // Level 1: the K loop of one workgroup (Eq. 2 over n_k K steps).
-    // element-aligned operands: the same 16-byte loads, but misaligned ones
-    // straddle an extra cache line per row segment and the ragged edge chunks
-    // are gathered element by element
-    const double load_factor = k.vec ? 1.0 : 1.25;
-    // (family 2 reads only B from memory in the loop; its A slice is loaded once)
-    const double xfer = (double)(valu ? k.nb : k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
-    const double t_load = hw.mem_latency_ns + xfer;
-    const double t_store = (double)k.mb * k.nb * eb / bw_wg + t_split_model;
-    const int depth = valu ? 1 : std::max(1, k.stages - 1);   // family 2: two register sets
-    double t1;
-    if (depth == 1 || nk <= 1) {
-        t1 = vx_cost_temporal(t_load, nk, cost0, t_store);
-    } else {
+        // Level 1: the K loop of one workgroup (Eq. 2 over n_k K steps).
+        // element-aligned operands: the same 16-byte loads, but misaligned ones
+        // straddle an extra cache line per row segment and the ragged edge chunks
+        // are gathered element by element
+        const double bw_wg = bw_wg_at(pc);
+        const double load_factor = k.vec ? 1.0 : 1.25;
+        // (family 2 reads only B from memory in the loop; its A slice is loaded once)
+        const double xfer = (double)(valu ? k.nb : k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
+        const double t_load = hw.mem_latency_ns + xfer;
+        const double t_store = (double)k.mb * k.nb * eb / bw_wg + (split_epilogue ? t_split_at(pc) : 0.0);
+        const int depth = valu ? 1 : std::max(1, k.stages - 1);   // family 2: two register sets
+        if (depth == 1 || nk_ <= 1)
+            return vx_cost_temporal(t_load, nk_, cost0, t_store);
         const double t_issue = std::max(xfer, t_load / depth);
-        t1 = t_load + (double)(nk - 1) * std::max(t_issue, cost0) + cost0 + t_store;
-    }
+        return t_load + (double)(nk_ - 1) * std::max(t_issue, cost0) + cost0 + t_store;
+    };
 
     // Level 2 (Eq. 4), dispatch constant, compulsory-traffic floor.
-    const double cost2 = (double)F * t1;
+    double cost2 = (double)F * t1_for(nk, split > 1, per_cu);
+    if (hyb)
+        cost2 += (double)F_dp * t1_for(nk_whole, false, (double)occ);
     return hw.launch_ns + std::max(cost2, floor_ns);
 }
 
@@ -209,6 +233,7 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
     const VxKernelEntry* reg = vxi_registry(&n);
     double best = INFINITY;
     int best_id = -1, best_split = 0, best_kps = 0;
+    int64_t best_dp = 0;
     for (int i = 0; i < n; ++i) {
         const vx_kernel_info& k = reg[i].info;
         if ((forced_id >= 0 && k.id != forced_id) || !vxi_wave_matches(f, k))
@@ -217,24 +242,38 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
             continue;
         if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || k.op != sh.op)
             continue;   // infeasible at every split (the same test opens vxi_cost)
-        for (int s : kSplits) {
-            int split = s;
-            if (forced_split > 0) {
-                if (s != 1)
-                    break;
-                // a forced split runs as the number of non-empty slices it yields
-                const int64_t kps0 = cdiv(cdiv(std::max<int64_t>(sh.K, 1), forced_split), k.kb) * k.kb;
-                split = sh.K == 0 ? 1 : (int)cdiv(sh.K, kps0);
+        // (split, hybrid grid) pairs: each split plain, then (split >= 2) hybrid
+        int pairs[2 * (int)(sizeof(kSplits) / sizeof(kSplits[0]))][2];
+        int np = 0;
+        if (forced_split != 0) {
+            // a forced split runs as the number of non-empty slices it yields
+            const int fs = forced_split < 0 ? -forced_split : forced_split;
+            const int64_t kps0 = cdiv(cdiv(std::max<int64_t>(sh.K, 1), fs), k.kb) * k.kb;
+            pairs[np][0] = sh.K == 0 ? 1 : (int)cdiv(sh.K, kps0);
+            pairs[np++][1] = forced_split < 0;
+        } else {
+            for (int s : kSplits) {
+                pairs[np][0] = s;
+                pairs[np++][1] = 0;
+                if (s >= 2 && f.hybrid) {
+                    pairs[np][0] = s;
+                    pairs[np++][1] = 1;
+                }
             }
+        }
+        for (int j = 0; j < np; ++j) {
+            const int split = pairs[j][0];
             int kps = 0;
-            const double c = vxi_cost(hw, sh, k, split, lim, &kps);
+            int64_t dp = 0;
+            const double c = vxi_cost(hw, sh, k, pairs[j][1] ? -split : split, lim, &kps, &dp);
             if (c < 0.0)
                 continue;
-            if (c < best) {   // strict: ties keep the earlier (lower id, smaller split) candidate
+            if (c < best) {   // strict: ties keep the earlier (lower id, smaller split, plain grid) candidate
                 best = c;
                 best_id = i;
                 best_split = split;
                 best_kps = kps;
+                best_dp = dp;
             }
         }
     }
@@ -248,9 +287,11 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
     p.c_vec = sh.c_vec;
     p.tiles_m = cdiv(sh.M, k.mb);
     p.tiles_n = cdiv(sh.N, k.nb);
-    p.grid = p.tiles_m * p.tiles_n * sh.batch * best_split;
+    const int64_t tiles = p.tiles_m * p.tiles_n * sh.batch;
+    p.dp_tiles = best_dp;
+    p.grid = best_dp + (tiles - best_dp) * best_split;
     p.group_m = vxi_group_m(p.tiles_m, p.tiles_n);
-    p.workspace_bytes = best_split > 1 ? (size_t)(p.tiles_m * p.tiles_n * sh.batch) * best_split * k.mb * k.nb * 4 : 0;
+    p.workspace_bytes = best_split > 1 ? (size_t)(tiles - best_dp) * best_split * k.mb * k.nb * 4 : 0;
     p.predicted_ns = best;
     p.kernel = k;
     *out = p;

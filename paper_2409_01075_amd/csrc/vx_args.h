@@ -14,7 +14,11 @@ struct VxGemmArgs {
     int batch;
     int group_m;            // tile rows walked together by the grid-level order
     int num_xcd;            // workgroups are dispatched round-robin over this many XCDs
-    int grid;               // workgroups in the launch: tiles_m * tiles_n * split * batch
+    int grid;               // workgroups in the launch: tiles_m * tiles_n * split * batch, or with
+                            // dp_tiles > 0, dp_tiles + (tiles_m * tiles_n * batch - dp_tiles) * split
+    int dp_tiles;           // > 0: hybrid grid -- the first dp_tiles tiles (whole waves of the
+                            // device, a multiple of num_xcd) run whole, one workgroup each; only
+                            // the remaining tiles are split `split` ways.  0: every tile is split.
     float* ws;              // split-K partial tiles (split > 1), fp32
     unsigned* tickets;      // one self-resetting arrival counter per output tile
     // 2-D convolution as an implicit GEMM (conv kernels only): A is the input

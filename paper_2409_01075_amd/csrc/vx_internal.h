@@ -51,17 +51,20 @@ struct VxLimits {
 // Resident workgroups per CU of kernel k (tighter of LDS and register budgets).
 int vxi_occupancy(const vx_hwinfo& hw, const vx_kernel_info& k);
 
-// Cost (ns) of kernel k with split s on shape sh; < 0 if infeasible.  On
-// success also returns the K extent per slice.
+// Cost (ns) of kernel k with split s on shape sh; < 0 if infeasible.  s < 0
+// asks for the hybrid grid (whole waves of whole tiles, the remaining tiles
+// split -s ways).  On success also returns the K extent per slice and the
+// number of whole tiles (0 for a plain grid).
 double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k, int split,
-                const VxLimits& lim, int* k_per_split);
+                const VxLimits& lim, int* k_per_split, int64_t* dp_tiles = nullptr);
 
 // Restrictions of the search, for tests and the hierarchy ablations.
 struct VxFilter {
     int kernel_id = -1;   // >= 0: only this kernel (a fixed workgroup and wavefront strategy)
-    int split = 0;        // > 0: only this split-K factor
+    int split = 0;        // > 0: only this split-K factor; < 0: only the hybrid grid with split -split
     int wave_m = 0, wave_n = 0, mfma_m = 0;   // > 0: only kernels with this wavefront strategy
     int backends = 3;     // bit 0: matrix-core (MFMA) kernels, bit 1: vector-ALU kernels
+    bool hybrid = true;   // the hybrid grid is among the plans considered
 };
 
 // True if kernel k passes the wavefront part of the filter.

@@ -41,7 +41,8 @@ class vx_conv2d_desc(ctypes.Structure):
 class vx_plan(ctypes.Structure):
     _fields_ = [("kernel_id", ctypes.c_int), ("split_k", ctypes.c_int), ("k_per_split", ctypes.c_int),
                 ("c_vec", ctypes.c_int), ("tiles_m", ctypes.c_int64), ("tiles_n", ctypes.c_int64),
-                ("grid", ctypes.c_int64), ("group_m", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t),
+                ("grid", ctypes.c_int64), ("dp_tiles", ctypes.c_int64), ("group_m", ctypes.c_int),
+                ("workspace_bytes", ctypes.c_size_t),
                 ("predicted_ns", ctypes.c_double), ("kernel", vx_kernel_info)]
 
 
@@ -90,6 +91,8 @@ def lib():
     L.vx_registry_count.restype = i32
     L.vx_registry_get.argtypes = [i32, ctypes.POINTER(vx_kernel_info)]
     L.vx_registry_get.restype = i32
+    L.vx_enable_hybrid_grid.argtypes = [i32]
+    L.vx_enable_hybrid_grid.restype = i32
     L.vx_force_plan.argtypes = [i32, i32]
     L.vx_force_plan.restype = i32
     L.vx_fix_wavefront.argtypes = [i32, i32, i32]
@@ -204,6 +207,10 @@ BACKEND_MFMA, BACKEND_VALU = 1, 2
 
 def vx_restrict_backends(mask=0):
     return lib().vx_restrict_backends(mask)
+
+
+def vx_enable_hybrid_grid(enable=1):
+    return lib().vx_enable_hybrid_grid(enable)
 
 
 def vx_set_workspace(ptr, nbytes, stream=None):

@@ -240,27 +240,35 @@ def test_selector_plans_cover_and_are_feasible(mi355x_override):
                     assert K % ve == 0 and N % ve == 0
                 assert p.tiles_m * k.mb >= M and (p.tiles_m - 1) * k.mb < M
                 assert p.tiles_n * k.nb >= N and (p.tiles_n - 1) * k.nb < N
-                assert p.grid == p.tiles_m * p.tiles_n * b * p.split_k
+                tiles = p.tiles_m * p.tiles_n * b
+                assert 0 <= p.dp_tiles < tiles
+                if p.dp_tiles:
+                    # hybrid grid: whole waves of whole tiles, the rest split
+                    occ = vx.vx_kernel_occupancy(p.kernel_id)
+                    assert p.split_k >= 2 and p.dp_tiles % (256 * occ) == 0
+                assert p.grid == p.dp_tiles + (tiles - p.dp_tiles) * p.split_k
                 if K == 0:
                     assert p.split_k == 1
                 else:
                     assert p.k_per_split % k.kb == 0
                     assert p.split_k * p.k_per_split >= K > (p.split_k - 1) * p.k_per_split
                 if p.split_k > 1:
-                    assert p.workspace_bytes == p.tiles_m * p.tiles_n * b * p.split_k * k.mb * k.nb * 4
+                    assert p.workspace_bytes == (tiles - p.dp_tiles) * p.split_k * k.mb * k.nb * 4
                     assert p.workspace_bytes <= 64 * 2 ** 20
                     assert p.tiles_m * p.tiles_n * b <= 65536
                 assert p.predicted_ns > 0
                 # deterministic
                 q = vx.vx_plan_query(b, M, N, K, dt, base_align=align)
-                assert (q.kernel_id, q.split_k) == (p.kernel_id, p.split_k)
+                assert (q.kernel_id, q.split_k, q.dp_tiles) == (p.kernel_id, p.split_k, p.dp_tiles)
 
 
 def test_selector_is_the_argmin_of_the_cost_model(mi355x_override):
     """Equation 1: the chosen plan has the lowest modelled cost of every
-    (kernel, split) pair, found here by brute force through vx_plan_cost."""
+    (kernel, split, grid) triple, found here by brute force through
+    vx_plan_cost (a negative split prices the hybrid grid)."""
     n = vx.vx_registry_count()
     splits = [1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32]
+    splits += [-s for s in splits if s > 1]
     for dt, (b, M, N, K) in [(1, (1, 1, 768, 768)), (1, (1, 300, 768, 768)), (2, (1, 8192, 4096, 4096)),
                              (2, (192, 333, 333, 64)), (2, (192, 336, 336, 64)), (0, (1, 77, 96, 80)), (2, (1, 16, 11008, 4096))]:
         p = vx.vx_plan_query(b, M, N, K, dt)
@@ -269,7 +277,7 @@ def test_selector_is_the_argmin_of_the_cost_model(mi355x_override):
         best = min(c for i in range(n) for s in splits
                    for st, c in [vx.vx_plan_cost(b, M, N, K, dt, i, s, vec_ok)] if st == 0)
         assert p.predicted_ns == pytest.approx(best, rel=1e-12)
-        st, c = vx.vx_plan_cost(b, M, N, K, dt, p.kernel_id, p.split_k, vec_ok)
+        st, c = vx.vx_plan_cost(b, M, N, K, dt, p.kernel_id, -p.split_k if p.dp_tiles else p.split_k, vec_ok)
         assert st == 0 and c == pytest.approx(p.predicted_ns, rel=1e-12)
 
 
@@ -409,3 +417,71 @@ def test_conv2d_large_image_avoids_32_bit_offsets(mi355x_override):
     small = vx.conv_desc(8, 256, 256, 64, 128, 3, 3, vx.VX_F16, pad=(1, 1))
     p = vx.vx_conv2d_plan_query(small)
     assert p.kernel.op == 1 and p.kernel.family == 1
+
+
+def test_hybrid_grid_plans(mi355x_override):
+    """The hybrid grid: whole waves of whole tiles plus the remaining tiles
+    split.  It exists only where the tiles exceed one wave of the device; it
+    is priced, forced and reported consistently."""
+    occ = {}
+    def slots(kid):
+        if kid not in occ:
+            occ[kid] = vx.vx_kernel_occupancy(kid)
+        return 256 * occ[kid]
+    # 6976 x 768 output, K = 3072: a hybrid candidate for every tile that leaves a partial wave
+    b, M, N, K, dt = 1, 6976, 768, 3072, 2
+    some = 0
+    for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count())):
+        if k.op or k.dtype != dt or not k.enabled:
+            continue
+        tiles = -(-M // k.mb) * -(-N // k.nb)
+        st, c = vx.vx_plan_cost(b, M, N, K, dt, k.id, -2, 1)
+        if tiles <= slots(k.id) or tiles % slots(k.id) == 0:
+            assert st == 3, (k.id, tiles)
+        elif st == 0:
+            some += 1
+            assert vx.vx_force_plan(k.id, -2) == 0
+            try:
+                p = vx.vx_plan_query(b, M, N, K, dt)
+            finally:
+                vx.vx_force_plan(-1, 0)
+            assert p.kernel_id == k.id and p.split_k == 2
+            assert p.dp_tiles == tiles // slots(k.id) * slots(k.id)
+            assert p.grid == p.dp_tiles + (tiles - p.dp_tiles) * 2
+            assert p.predicted_ns == pytest.approx(c, rel=1e-12)
+    assert some > 10
+    # one wave or less: no hybrid grid, forced or chosen
+    k = vx.vx_plan_query(1, 128, 128, 4096, dt).kernel
+    assert vx.vx_force_plan(k.id, -2) == 0
+    try:
+        with pytest.raises(vx.VxError):
+            vx.vx_plan_query(1, 128, 128, 4096, dt)
+    finally:
+        vx.vx_force_plan(-1, 0)
+    assert vx.vx_plan_query(1, 128, 128, 4096, dt).dp_tiles == 0
+
+
+def test_hybrid_grid_ablation_switch(mi355x_override):
+    """vx_enable_hybrid_grid(0) takes the hybrid grid out of the selector's
+    choices (and 1 puts it back); forced plans are not affected."""
+    found = None
+    for (M, N, K) in ((4904, 4096, 11008), (2544, 4096, 11008), (8192, 11008, 4096), (6976, 768, 3072)):
+        p = vx.vx_plan_query(1, M, N, K, 2)
+        if p.dp_tiles:
+            found = (M, N, K)
+            break
+    if found is None:
+        pytest.skip("no hybrid plan among these shapes for this calibration")
+    try:
+        assert vx.vx_enable_hybrid_grid(0) == 0
+        q = vx.vx_plan_query(1, *found, 2)
+        assert q.dp_tiles == 0 and q.predicted_ns >= p.predicted_ns
+        assert vx.vx_force_plan(p.kernel_id, -p.split_k) == 0
+        try:
+            f = vx.vx_plan_query(1, *found, 2)
+        finally:
+            vx.vx_force_plan(-1, 0)
+        assert f.dp_tiles == p.dp_tiles and f.predicted_ns == pytest.approx(p.predicted_ns, rel=1e-12)
+    finally:
+        assert vx.vx_enable_hybrid_grid(1) == 0
+    assert vx.vx_plan_query(1, *found, 2).dp_tiles == p.dp_tiles

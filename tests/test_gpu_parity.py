@@ -308,3 +308,90 @@ def test_error_codes_on_device():
     # C overlapping A
     assert vx.vx_gemm(4, 4, 4, 1, x.data_ptr(), x.data_ptr() + 64, x.data_ptr() + 8, s) == 1
     assert vx.vx_force_plan(10 ** 6, 1) == 3
+
+
+def _hybrid_shape(k, code):
+    """(M, N, tiles): an output one wave of kernel k's workgroups plus about a
+    third of a wave, ragged in both directions."""
+    num_cu = vx.vx_get_hwinfo().num_cu
+    slots = num_cu * vx.vx_kernel_occupancy(k.id)
+    target = slots + slots // 3 + 1
+    tiles_n = max(2, min(16, target // 8))
+    tiles_m = -(-target // tiles_n)
+    M = tiles_m * k.mb - 3
+    N = tiles_n * k.nb - (8 if k.vec else 5)
+    return M, N, tiles_m * tiles_n
+
+
+def _tile_samples(g, M, N, mb, nb):
+    """One random position in every output tile, plus the last row and column."""
+    rows, cols = [], []
+    for tm in range(-(-M // mb)):
+        for tn in range(-(-N // nb)):
+            rows.append(min(M - 1, tm * mb + int(g.integers(0, mb))))
+            cols.append(min(N - 1, tn * nb + int(g.integers(0, nb))))
+    rows += [M - 1] * 4 + list(g.integers(0, M, 4))
+    cols += list(g.integers(0, N, 4)) + [N - 1] * 4
+    return np.array(rows), np.array(cols)
+
+
+@pytest.mark.parametrize("code", DTS)
+def test_hybrid_grid_integer_exact(code):
+    """The hybrid grid (whole waves of whole tiles, then the remaining tiles
+    split into slices reduced by the last arrival) forced on kernels of each
+    family: exact on integer inputs at one position of every tile, the same
+    bits on a second call (the counters of the split tiles reset themselves)."""
+    g = I.rng(900 + code)
+    ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled]
+    picked = {}
+    for k in ks:
+        picked.setdefault((k.family, k.vec, k.mb * k.nb >= 128 * 128), k)
+    ran = 0
+    for k in picked.values():
+        M, N, tiles = _hybrid_shape(k, code)
+        for split in (2, 3):
+            K = 2 * split * k.kb + (8 if k.vec else 5)
+            if k.k_max and K > k.k_max:
+                continue
+            r = max(1, min(3, I.exact_range(K, code)))
+            A = I.small_int(g, (M, K), code, -r, r)
+            B = I.small_int(g, (K, N), code, -r, r)
+            assert vx.vx_force_plan(k.id, -split) == 0
+            try:
+                p = vx.vx_plan_query(1, M, N, K, code, M * K, K * N, M * N)
+                assert p.dp_tiles > 0 and p.split_k == split and p.grid == p.dp_tiles + (tiles - p.dp_tiles) * split
+                C1 = run_gemm(A, B, code)
+                C2 = run_gemm(A, B, code)
+            finally:
+                vx.vx_force_plan(-1, 0)
+            rows, cols = _tile_samples(g, M, N, k.mb, k.nb)
+            ref, _ = oracle.gemm_sampled(A, B, code, M, N, K, rows, cols)
+            tolerance.check_exact(C1[rows, cols], ref, code, "hybrid kernel %d split %d %dx%dx%d" % (k.id, split, M, N, K))
+            assert np.array_equal(C1, C2)
+            ran += 1
+    assert ran >= 3
+
+
+@pytest.mark.parametrize("code", [1, 2])
+def test_hybrid_grid_random_within_bound(code):
+    """The encoder's (M x 3072) x (3072 x 768) GEMM at M = 6976 with the hybrid
+    grid forced on the 128 x 128 kernels for which it exists (330 tiles), random
+    operands, sampled check."""
+    g = I.rng(950 + code)
+    M, N, K = 6976, 768, 3072
+    A = I.normal(g, (M, K), code)
+    B = I.normal(g, (K, N), code, 0.02)
+    ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and k.vec and k.mb == 128 and k.nb == 128
+          and vx.vx_plan_cost(1, M, N, K, code, k.id, -3, 1)[0] == 0]
+    assert ks
+    k = ks[0]
+    assert vx.vx_force_plan(k.id, -3) == 0
+    try:
+        p = vx.vx_plan_query(1, M, N, K, code)
+        C = run_gemm(A, B, code)
+    finally:
+        vx.vx_force_plan(-1, 0)
+    assert p.dp_tiles > 0 and p.split_k == 3
+    rows, cols = _tile_samples(g, M, N, k.mb, k.nb)
+    ref, mag = oracle.gemm_sampled(A, B, code, M, N, K, rows, cols)
+    tolerance.check(C[rows, cols], ref, mag, code, "hybrid kernel %d" % k.id)
