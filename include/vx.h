@@ -100,6 +100,10 @@ typedef struct vx_kernel_info {
                                       keeps its slice of A in LDS */
     int op;                        /* 0: GEMM; 1: 2-D convolution (implicit GEMM: A is the input
                                       image read through the im2col map) */
+    int schedule;                  /* family 1, level-1 DMA issue: 0 every wave issues its share of
+                                      each K step; 1 ping-pong (8 waves, 2 stages): the two halves
+                                      of the waves take turns issuing whole K steps while the other
+                                      half starts its MFMAs */
 } vx_kernel_info;
 
 /* A concrete execution plan for one call. */

@@ -259,7 +259,7 @@ def _entry(dtype, family, stages, c, vec, hw):
     mb, nb, kb, wm, wn, mi = c
     lds = lds_bytes_dma(mb, nb, kb, stages) if family == "dma" else lds_bytes(dtype, mb, nb, kb)
     return dict(dtype=dtype, dt=DT_CODE[dtype], family=family, stages=stages, mb=mb, nb=nb, kb=kb, wm=wm,
-                wn=wn, mi=mi, vec=vec, threads=wm * wn * hw["wave"], lds=lds, k_max=0, op=0)
+                wn=wn, mi=mi, vec=vec, threads=wm * wn * hw["wave"], lds=lds, k_max=0, op=0, schedule=0)
 
 
 # ------------------------------------------------ convolution (implicit GEMM) --
@@ -345,6 +345,25 @@ def valu_candidates(dtype, hw=GFX950):
     return out
 
 
+# Ping-pong DMA issue (direct-to-LDS, 8 waves, 2-stage ring): instead of every
+# wave issuing its share of the next K step right after the barrier (all
+# eight then wait on the CU's load path together, with the matrix cores
+# idle), the two halves of the waves -- one wave per SIMD each -- take turns
+# issuing whole K steps, and the other half starts its MFMAs at once.
+def pingpong_candidates(base):
+    out = []
+    for e in base:
+        if e["family"] == "dma" and e["op"] == 0 and e["stages"] == 2 and e["wm"] * e["wn"] == 8:
+            a_instr = e["mb"] * e["kb"] * 2 // 1024
+            b_instr = e["kb"] * e["nb"] * 2 // 1024
+            if a_instr % 4 or b_instr % 4 or 2 * (a_instr + b_instr) // 8 > 63:
+                continue
+            p = dict(e)
+            p["schedule"] = 1
+            out.append(p)
+    return out
+
+
 def registry(hw=GFX950):
     """All workgroup-level candidates that are compiled into the library.
 
@@ -376,6 +395,7 @@ def registry(hw=GFX950):
         out += conv_dma_candidates(dtype, hw)
     for dtype in ("f16", "bf16"):
         out += dma_wide_candidates(dtype, hw)
+    out += pingpong_candidates(list(out))
     for i, e in enumerate(out):
         e["id"] = i
     return out

@@ -27,11 +27,15 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
-template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_, bool CONV_ = false>
+template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_, bool CONV_ = false,
+          bool PP_ = false>
 struct DCfg {
     static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_, STAGES = ST_;
     static constexpr bool VEC = VEC_;
     static constexpr bool CONV = CONV_;   // A is an image read through the im2col map
+    // ping-pong issue: the waves [0, 4) and [4, 8) -- one per SIMD each -- take
+    // turns issuing a whole K step; the other half starts its MFMAs at once
+    static constexpr bool PP = PP_;
     static constexpr bool H = true;
     static constexpr int EB = 2;
     static constexpr int NWAVE = WM * WN, NT = NWAVE * 64;
@@ -67,6 +71,9 @@ struct DCfg {
     static_assert((STAGES - 1) * LPS <= 63, "vmcnt range: the prologue's DMA all in flight");
     static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
     static_assert(!CONV || CPA == 8, "convolution: one 128-byte row segment per 8 lanes (Kb = 64)");
+    static_assert(!PP || (NWAVE == 8 && STAGES == 2 && !CONV && 2 * LPS <= 63 && (A_BYTES / WAVE_BYTES) % 4 == 0 &&
+                          (B_BYTES / WAVE_BYTES) % 4 == 0),
+                  "ping-pong: 8 waves, a 2-stage ring, K steps split evenly over 4 issuing waves");
 };
 
 __device__ __forceinline__ int swz_a(int r, int period) { return r & (period - 1); }
@@ -208,12 +215,18 @@ struct DmaConvA {
     }
 };
 
-template <class C>
+template <class C, int NI = C::NWAVE>
 struct DmaTile {
-    // The DMA of one K step (starting at k0) into one LDS stage: LPS
-    // instructions per wave, A's A_IPW first, then B's B_IPW.  A step can be
-    // issued whole (issue) or one instruction at a time (one<I>), so that the
-    // main loop can spread it between the MFMAs of the step being computed.
+    // The DMA of one K step (starting at k0) into one LDS stage, issued by NI
+    // waves: LPS instructions per wave, A's A_IPW first, then B's B_IPW.  A
+    // step can be issued whole (issue) or one instruction at a time (one<I>),
+    // so that the main loop can spread it between the MFMAs of the step being
+    // computed.
+    static constexpr int A_IPW = C::A_BYTES / C::WAVE_BYTES / NI;
+    static constexpr int B_IPW = C::B_BYTES / C::WAVE_BYTES / NI;
+    static constexpr int LPS = A_IPW + B_IPW;
+    static_assert(A_IPW * NI * C::WAVE_BYTES == C::A_BYTES && B_IPW * NI * C::WAVE_BYTES == C::B_BYTES,
+                  "the step splits evenly over the issuing waves");
     lds_char* stage;
     u32x4 ra, rb;   // A resource at column k0 of the panel; B resource at row k0, column n0
     int kv, nv;     // valid columns of A from k0; valid columns of B from n0
@@ -244,21 +257,21 @@ struct DmaTile {
     template <int I>
     __device__ __forceinline__ void one(int Mrel, int N, int K, int wave, int lane) const
     {
-        if constexpr (I < C::A_IPW && C::CONV) {
+        if constexpr (I < A_IPW && C::CONV) {
             // A: the taps of this lane's output pixel I at this step's columns
-            const int instr = wave * C::A_IPW + I;
+            const int instr = wave * A_IPW + I;
             const bool ok = kin && (unsigned)(cv->ih0[I] + dh) < (unsigned)cH && (unsigned)(cv->iw0[I] + dw) < (unsigned)cW;
             dma_lds<C::LANE_BYTES>(ra, stage + instr * C::WAVE_BYTES, ok ? (cv->pix[I] + koff) * 2u : kOOB);
-        } else if constexpr (I < C::A_IPW) {
+        } else if constexpr (I < A_IPW) {
             // A: rows of the workgroup's panel
-            const int instr = wave * C::A_IPW + I;
+            const int instr = wave * A_IPW + I;
             const int slot = instr * 64 + lane;                  // chunk index in the stage
             const int r = slot / C::CPA, c = (slot % C::CPA) ^ swz_a(r, C::SWA);
             const bool ok = r < Mrel && c * 8 < kv;
             dma_lds<C::LANE_BYTES>(ra, stage + instr * C::WAVE_BYTES, ok ? (unsigned)((r * K + c * 8) * 2) : kOOB);
         } else {
             // B: rows k0.. of the batch's B, columns from n0
-            const int instr = wave * C::B_IPW + (I - C::A_IPW);
+            const int instr = wave * B_IPW + (I - A_IPW);
             const int slot = instr * 64 + lane;
             const int k = slot / C::CPB, c = b_chunk<C::CPB>(slot % C::CPB, k);
             const bool ok = k < kv && c * 8 < nv;
@@ -279,7 +292,7 @@ struct DmaTile {
 
     __device__ __forceinline__ void issue(int Mrel, int N, int K, int wave, int lane) const
     {
-        range<0, C::LPS>(Mrel, N, K, wave, lane);
+        range<0, LPS>(Mrel, N, K, wave, lane);
     }
 };
 
@@ -424,18 +437,44 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
     for (int s = 0; s < C::STAGES - 1; ++s)
         if (s < g.nk)
             tile(VX_STAGE(s), g.kbeg + s * C::KB).issue(Mrel, p.N, p.K, wave, lane);
-    // main loop, unrolled by STAGES so that every stage index is a constant
-    for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
+    if constexpr (C::PP) {
+        // Ping-pong (2 stages): step 0 came from every wave above; then at
+        // step it the half (wave >> 2) == it % 2 issues step it+1 whole into
+        // the other stage while the other half starts its MFMAs right after
+        // the barrier.  A wave waits only for what it issued itself.
+        const DmaTile<C> none(VX_STAGE(0), Apanel, Bbatch, g.kbeg, g.kend, g.n0, p.N);
+        for (int it0 = 0; it0 < g.nk; it0 += 2) {
 #pragma unroll
-        for (int j = 0; j < C::STAGES; ++j) {
-            const int it = it0 + j;
-            if (it >= g.nk)
-                break;
-            wait_steps<C::LPS, C::STAGES - 2>(g.nk - 1 - it);   // step `it` has landed (this wave's part)
-            __builtin_amdgcn_s_barrier();                      // ... and every wave's; stage it-1 is free
-            // step it+STAGES-1 goes into the freed stage, issued between the MFMAs of step it
-            const DmaTile<C> next = tile(VX_STAGE((j + C::STAGES - 1) % C::STAGES), g.kbeg + (it + C::STAGES - 1) * C::KB);
-            dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, next, it + C::STAGES - 1 < g.nk, Mrel, p.N, p.K, wave);
+            for (int j = 0; j < 2; ++j) {
+                const int it = it0 + j;
+                if (it >= g.nk)
+                    break;
+                wait_vm<0>();                  // step it has landed (the part this wave issued, if any)
+                __builtin_amdgcn_s_barrier();  // ... and every wave's; stage j ^ 1 is free
+                if (it + 1 < g.nk && (wave >> 2) == j)
+                    DmaTile<C, C::NWAVE / 2>(VX_STAGE(j ^ 1), Apanel, Bbatch, g.kbeg + (it + 1) * C::KB, g.kend, g.n0,
+                                             p.N)
+                        .issue(Mrel, p.N, p.K, wave & 3, lane);
+                __builtin_amdgcn_sched_barrier(0);
+                dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, none, false, Mrel, p.N, p.K, wave);
+            }
+        }
+    } else {
+        // main loop, unrolled by STAGES so that every stage index is a constant
+        for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
+#pragma unroll
+            for (int j = 0; j < C::STAGES; ++j) {
+                const int it = it0 + j;
+                if (it >= g.nk)
+                    break;
+                wait_steps<C::LPS, C::STAGES - 2>(g.nk - 1 - it);   // step `it` has landed (this wave's part)
+                __builtin_amdgcn_s_barrier();                      // ... and every wave's; stage it-1 is free
+                // step it+STAGES-1 goes into the freed stage, issued between the MFMAs of step it
+                const DmaTile<C> next =
+                    tile(VX_STAGE((j + C::STAGES - 1) % C::STAGES), g.kbeg + (it + C::STAGES - 1) * C::KB);
+                dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, next, it + C::STAGES - 1 < g.nk, Mrel, p.N, p.K,
+                               wave);
+            }
         }
     }
     wait_vm<0>();   // nothing is in flight here; kept as a guard before LDS is released

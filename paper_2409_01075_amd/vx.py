@@ -30,7 +30,7 @@ class vx_kernel_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in (
         "id", "dtype", "mb", "nb", "kb", "wm", "wn", "mfma_m", "mfma_n", "mfma_k", "vec", "family", "stages",
         "threads",
-        "lds_bytes", "vgprs", "agprs", "sgprs", "scratch_bytes", "enabled", "k_max", "op")]
+        "lds_bytes", "vgprs", "agprs", "sgprs", "scratch_bytes", "enabled", "k_max", "op", "schedule")]
 
 
 class vx_conv2d_desc(ctypes.Structure):
