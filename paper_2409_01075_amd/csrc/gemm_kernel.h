@@ -502,29 +502,33 @@ __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
     // Workgroups are dispatched round-robin over the XCDs; remap the linear id
     // so that each XCD receives a contiguous range of logical tiles
     // (neighbouring tiles share A or B panels in that XCD's L2).
-    // A hybrid grid remaps its two classes of workgroups -- the whole tiles
-    // [0, dp_tiles), dispatched first, and the split tiles' slices after them
-    // -- each on its own; dp_tiles is a multiple of num_xcd, so a workgroup's
-    // XCD is its index within the class modulo num_xcd as well.
     const int w = blockIdx.x;
     const int nx = p.num_xcd;
-    const bool hyb = p.dp_tiles > 0;
-    const bool whole = hyb && w < p.dp_tiles;
-    const int wc = hyb && !whole ? w - p.dp_tiles : w;
-    const int G = hyb ? (whole ? p.dp_tiles : p.grid - p.dp_tiles) : p.grid;
-    const int xcd = wc % nx, q = G / nx, rem = G % nx;
-    const int wl = xcd * q + (xcd < rem ? xcd : rem) + wc / nx;
-
     GridPos g;
     g.tiles = p.tiles_m * p.tiles_n;
     int tile;
-    if (!hyb) {
+    bool whole = false;
+    if (p.dp_tiles == 0) {
+        // plain grid: every tile in split slices
+        const int G = p.grid;
+        const int xcd = w % nx, q = G / nx, rem = G % nx;
+        const int wl = xcd * q + (xcd < rem ? xcd : rem) + w / nx;
         tile = wl % g.tiles;
         const int bz = wl / g.tiles;
         g.z = bz % p.split;
         g.b = bz / p.split;
         g.split = p.split;
     } else {
+        // hybrid grid: its two classes of workgroups -- the whole tiles
+        // [0, dp_tiles), dispatched first, and the split tiles' slices after
+        // them -- are remapped each on its own; dp_tiles is a multiple of
+        // num_xcd, so a workgroup's XCD is its index within the class modulo
+        // num_xcd as well
+        whole = w < p.dp_tiles;
+        const int wc = whole ? w : w - p.dp_tiles;
+        const int G = whole ? p.dp_tiles : p.grid - p.dp_tiles;
+        const int xcd = wc % nx, q = G / nx, rem = G % nx;
+        const int wl = xcd * q + (xcd < rem ? xcd : rem) + wc / nx;
         const int rt = p.batch * g.tiles - p.dp_tiles;   // tiles that are split
         const int T = whole ? wl : p.dp_tiles + wl % rt;
         g.z = whole ? 0 : wl / rt;
@@ -542,7 +546,7 @@ __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
     g.tn = (tile % per_group) / gm;
     g.m0 = g.tm * MB;
     g.n0 = g.tn * NB;
-    if (!hyb)
+    if (p.dp_tiles == 0)
         g.rid = g.b * g.tiles + g.tm * p.tiles_n + g.tn;
     g.kbeg = whole ? 0 : g.z * p.k_per_split;
     g.kend = whole ? p.K : min(p.K, g.kbeg + p.k_per_split);

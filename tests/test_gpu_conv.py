@@ -105,3 +105,42 @@ def test_conv_zero_channels_and_empty_output():
     x = torch.ones((1, 2, 2, 8), dtype=torch.float16, device=dev)
     w = torch.ones((5, 5, 8, 8), dtype=torch.float16, device=dev)
     assert vx.conv2d(x, w).numel() == 0
+
+
+@pytest.mark.parametrize("code", [1, 2])
+def test_conv_hybrid_grid_integer_exact(code):
+    """A convolution whose implicit GEMM has more tiles than one wave of the
+    device (the image sized for the kernel), with the hybrid grid forced on a
+    direct-to-LDS and a register-staged convolution kernel: exact on integer
+    inputs, and the same bits on a second call."""
+    g = I.rng(1400 + code)
+    num_cu = vx.vx_get_hwinfo().num_cu
+    Cin, KH, KW = 16, 3, 3
+    ran = 0
+    for fam in (1, 0):
+        k = next(k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count()))
+                 if k.op == 1 and k.dtype == code and k.enabled and k.family == fam)
+        slots = num_cu * vx.vx_kernel_occupancy(k.id)
+        Cout = 2 * k.nb - 8                                  # two tile columns, the second ragged
+        tiles_m = -(-(slots + slots // 3 + 1) // 2)
+        H = 32
+        W = -(-(tiles_m * k.mb - k.mb // 2) // H)             # M = H * W, the last tile row ragged
+        M = H * W
+        tiles = -(-M // k.mb) * 2
+        assert tiles > slots and tiles % slots != 0
+        x = I.small_int(g, (1, H, W, Cin), code, -2, 2)
+        w = I.small_int(g, (KH, KW, Cin, Cout), code, -2, 2)
+        ref = oracle.conv2d(x, w, code, (1, 1), (1, 1), (1, 1), with_mag=False)
+        assert vx.vx_force_plan(k.id, -2) == 0
+        try:
+            d = vx.conv_desc(1, H, W, Cin, Cout, KH, KW, code, pad=(1, 1))
+            p = vx.vx_conv2d_plan_query(d)
+            assert p.dp_tiles > 0 and p.split_k == 2
+            y1 = run_conv(x, w, code, (1, 1), (1, 1), (1, 1))
+            y2 = run_conv(x, w, code, (1, 1), (1, 1), (1, 1))
+        finally:
+            vx.vx_force_plan(-1, 0)
+        tolerance.check_exact(y1, ref, code, "conv hybrid kernel %d" % k.id)
+        assert np.array_equal(y1, y2)
+        ran += 1
+    assert ran == 2
