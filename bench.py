@@ -324,14 +324,15 @@ def run_study(args):
         label, b, M, N, K, dt, mk = job
         eb = 4 if dt == 0 else 2
         ve = 16 // eb
-        vec_ok = int(K % ve == 0 and N % ve == 0 and (b == 1 or (M * K) % ve == 0))
+        vec_ok = (int(K % ve == 0 and (b == 1 or (M * K) % ve == 0))
+                  | 2 * int(N % ve == 0 and (b == 1 or (K * N) % ve == 0)))   # rows aligned: bit 0 A, bit 1 B
         call, R, keep = _study_ctx(job, dev, args.rot_mib, L, sp)
         plan = vx.vx_plan_query(b, M, N, K, dt, M * K, K * N, M * N)
         call(0)
         t_pick = _time_calls(call, R, stream, spin)
         table = {}
         for k in reg:
-            if k.op != 0 or k.dtype != dt or not k.enabled or (k.vec and not vec_ok):
+            if k.op != 0 or k.dtype != dt or not k.enabled or (k.align & ~vec_ok):
                 continue
             for split in (1, 2, 4, 8, -2, -4):   # negative: the hybrid grid
                 st, _ = vx.vx_plan_cost(b, M, N, K, dt, k.id, split, vec_ok)

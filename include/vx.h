@@ -85,7 +85,7 @@ typedef struct vx_kernel_info {
     int mb, nb, kb;                /* workgroup tile */
     int wm, wn;                    /* wavefront grid; wavefront tile = (mb/wm) x (nb/wn) */
     int mfma_m, mfma_n, mfma_k;    /* instruction tile (0 for the vector-ALU family) */
-    int vec;                       /* 1: needs 16-byte-aligned operand rows; 0: any element alignment */
+    int vec;                       /* 1: needs 16-byte-aligned rows of A and B; 0: not both (see align) */
     int family;                    /* 0: MFMA, loads staged through registers; 1: MFMA, direct-to-LDS
                                       DMA; 2: vector ALU (v_dot2 / v_fma), B rows straight to VGPRs,
                                       for small M (mb = the rows one workgroup covers) */
@@ -100,6 +100,9 @@ typedef struct vx_kernel_info {
                                       keeps its slice of A in LDS */
     int op;                        /* 0: GEMM; 1: 2-D convolution (implicit GEMM: A is the input
                                       image read through the im2col map) */
+    int align;                     /* rows that must start on 16-byte boundaries: bit 0 A's, bit 1
+                                      B's (family 1 moves such an operand by DMA, the other through
+                                      VGPRs) */
     int schedule;                  /* family 1, level-1 DMA issue: 0 every wave issues its share of
                                       each K step; 1 ping-pong (8 waves, 2 stages): the two halves
                                       of the waves take turns issuing whole K steps while the other
@@ -155,9 +158,11 @@ vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype
  * The cost model's estimate (ns) for running a given kernel with a given
  * split-K factor on a shape; VX_ERR_NO_CANDIDATE if the pair is infeasible.
  * split_k < 0 prices the hybrid grid with -split_k slices per split tile.
+ * align: which operands' rows start on 16-byte boundaries (bit 0 A, bit 1 B;
+ * 3 both, 0 neither); VX_ERR_INVALID_ARG outside 0..3.
  */
 vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype,
-                       int kernel_id, int split_k, int vec_ok, double* out_ns);
+                       int kernel_id, int split_k, int align, double* out_ns);
 
 /* Equation 2: T = t_load + (trips - 1) * max(t_load, cost_lower) + cost_lower + t_store
  * (trips >= 1; trips == 0 gives t_store). */

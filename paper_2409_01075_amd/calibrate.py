@@ -92,14 +92,16 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
         def timed(M, N, K, split):
             set_bytes = (M * K + K * N + M * N) * eb
             R = int(min(max(2, -(-rot_mib * 2 ** 20 // set_bytes)), 512))
-            # element-aligned kernels are timed on operands shifted by one
-            # element, so that every row access is the misaligned kind they
-            # exist for
-            sh = 0 if k.vec else 1
-            A = torch.randn((R * M * K + sh,), device=dev).to(tdt[k.dtype])
-            B = torch.randn((R * K * N + sh,), device=dev).to(tdt[k.dtype])
-            C = torch.empty((R * M * N + sh,), dtype=tdt[k.dtype], device=dev)
-            a0, b0, cc = (X.data_ptr() + sh * eb for X in (A, B, C))
+            # an operand whose rows the kernel does not need aligned is timed
+            # shifted by one element, so that every row access is the
+            # misaligned kind the kernel exists for
+            sha = 0 if k.align & 1 else 1
+            shb = 0 if k.align & 2 else 1
+            shc = 0 if k.vec else 1
+            A = torch.randn((R * M * K + sha,), device=dev).to(tdt[k.dtype])
+            B = torch.randn((R * K * N + shb,), device=dev).to(tdt[k.dtype])
+            C = torch.empty((R * M * N + shc,), dtype=tdt[k.dtype], device=dev)
+            a0, b0, cc = A.data_ptr() + sha * eb, B.data_ptr() + shb * eb, C.data_ptr() + shc * eb
             sa, sb, sc = M * K * eb, K * N * eb, M * N * eb
             vx.vx_force_plan(kid, split)
             # a convolution kernel runs the same implicit-GEMM shape as a 1 x 1

@@ -311,9 +311,10 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
     sh.K = K;
     sh.dt = dtype;
     const int ve = 16 / eb;
-    const bool strides_vec = batch == 1 || ((sA % ve) == 0 && (sB % ve) == 0);
-    sh.vec_ok = (K % ve == 0) && (N % ve == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) &&
-                strides_vec;
+    // per operand: every row starts on a 16-byte boundary
+    const bool a_vec = (K % ve == 0) && ((uintptr_t)A % 16 == 0) && (batch == 1 || sA % ve == 0);
+    const bool b_vec = (N % ve == 0) && ((uintptr_t)B % 16 == 0) && (batch == 1 || sB % ve == 0);
+    sh.vec_ok = (a_vec ? 1 : 0) | (b_vec ? 2 : 0);
     sh.c_vec = (N % 4 == 0) && ((uintptr_t)C % (4 * eb) == 0) && (batch == 1 || sC % 4 == 0);
 
     VxGemmArgs a = {};
@@ -423,7 +424,7 @@ vx_status conv_shape(const vx_conv2d_desc* d, VxShape* sh, VxGemmArgs* a, bool* 
     // image offsets are 32-bit (operand alignment is checked by the caller
     // that has the pointers); vec_ok is part of the plan cache's key
     sh->a_bytes = (int64_t)((double)d->n * d->h * d->w * d->c_in) * elem_bytes(d->dtype);
-    sh->vec_ok = d->dtype != VX_F32 && d->c_in % 8 == 0 && d->c_out % 8 == 0 && sh->a_bytes < ((int64_t)1 << 31);
+    sh->vec_ok = d->dtype != VX_F32 && d->c_in % 8 == 0 && d->c_out % 8 == 0 && sh->a_bytes < ((int64_t)1 << 31) ? 3 : 0;
     sh->c_vec = 0;
     sh->op = 1;
     a->cH = (int)d->h;
@@ -549,8 +550,9 @@ vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype
     sh.N = N;
     sh.K = K;
     sh.dt = dtype;
-    const bool strides_vec = batch == 1 || ((strideA % ve) == 0 && (strideB % ve) == 0);
-    sh.vec_ok = (K % ve == 0) && (N % ve == 0) && (base_align % 16 == 0) && strides_vec;
+    const bool a_vec = (K % ve == 0) && (base_align % 16 == 0) && (batch == 1 || strideA % ve == 0);
+    const bool b_vec = (N % ve == 0) && (base_align % 16 == 0) && (batch == 1 || strideB % ve == 0);
+    sh.vec_ok = (a_vec ? 1 : 0) | (b_vec ? 2 : 0);
     sh.c_vec = (N % 4 == 0) && (base_align % (4 * eb) == 0) && (batch == 1 || strideC % 4 == 0);
     int dev = 0;
     vx_status st = current_device(&dev);
@@ -576,7 +578,7 @@ vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void*
         return VX_ERR_INVALID_ARG;
     if (empty)
         return VX_OK;
-    sh.vec_ok = sh.vec_ok && (uintptr_t)x % 16 == 0 && (uintptr_t)w % 16 == 0;
+    sh.vec_ok = sh.vec_ok && (uintptr_t)x % 16 == 0 && (uintptr_t)w % 16 == 0 ? 3 : 0;
     a.A = x;
     a.B = w;
     a.C = y;
@@ -601,7 +603,7 @@ vx_status vx_conv2d_plan_query(const vx_conv2d_desc* d, vx_plan* out)
 }
 
 vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, int kernel_id,
-                       int split_k, int vec_ok, double* out_ns)
+                       int split_k, int align, double* out_ns)
 {
     if (dtype != VX_F32 && dtype != VX_F16 && dtype != VX_BF16)
         return VX_ERR_UNSUPPORTED_DTYPE;
@@ -619,7 +621,9 @@ vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype 
     st = hwinfo_for(dev, &hw);
     if (st != VX_OK)
         return st;
-    VxShape sh{batch, M, N, K, (int)dtype, vec_ok ? 1 : 0, 1};
+    if (align < 0 || align > 3)
+        return VX_ERR_INVALID_ARG;
+    VxShape sh{batch, M, N, K, (int)dtype, align, 1};
     VxLimits lim{kDefaultPartials, (int64_t)(kTicketBytes / 4)};
     const double c = vxi_cost(hw, sh, reg[kernel_id].info, split_k, lim, nullptr);
     if (c < 0.0)

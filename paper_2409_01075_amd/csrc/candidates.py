@@ -364,6 +364,37 @@ def pingpong_candidates(base):
     return out
 
 
+# Mixed loads (fp16/bf16): one operand by DMA, the other -- whose rows need not
+# start on 16-byte boundaries (an odd K for A, an odd N for B, or such a batch
+# stride) -- through VGPRs into the same LDS layout.  A GEMM with one misaligned
+# operand then keeps the DMA for the other instead of falling back to the
+# register-staged family for both.  Kb = 64, 2-stage rings, one wave layout
+# per workgroup tile (the first the generator lists).
+MIXED_TILES = {(32, 64), (64, 32), (64, 64), (128, 64), (64, 128), (128, 128), (256, 64), (64, 256), (256, 128),
+               (128, 256), (256, 256)}
+
+
+def mixed_candidates(base, hw=GFX950):
+    out, seen = [], set()
+    for e in base:
+        if e["family"] != "dma" or e["op"] or e["stages"] != 2 or e.get("schedule", 0) or e["kb"] != 64:
+            continue
+        if (e["mb"], e["nb"]) not in MIXED_TILES or (e["dtype"], e["mb"], e["nb"]) in seen:
+            continue
+        nt = e["wm"] * e["wn"] * hw["wave"]
+        for vg in (1, 2):
+            chunks = e["mb"] * (e["kb"] // 8) if vg == 1 else e["kb"] * (e["nb"] // 8)
+            if chunks % nt or chunks // nt > 16:
+                continue
+            m = dict(e)
+            m["vg"] = vg
+            m["vec"] = 0
+            m["align"] = 2 if vg == 1 else 1
+            out.append(m)
+        seen.add((e["dtype"], e["mb"], e["nb"]))
+    return out
+
+
 def registry(hw=GFX950):
     """All workgroup-level candidates that are compiled into the library.
 
@@ -396,6 +427,7 @@ def registry(hw=GFX950):
     for dtype in ("f16", "bf16"):
         out += dma_wide_candidates(dtype, hw)
     out += pingpong_candidates(list(out))
+    out += mixed_candidates(list(out), hw)
     for i, e in enumerate(out):
         e["id"] = i
     return out

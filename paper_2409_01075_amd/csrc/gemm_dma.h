@@ -28,7 +28,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_, bool CONV_ = false,
-          bool PP_ = false>
+          bool PP_ = false, int VG_ = 0>
 struct DCfg {
     static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_, STAGES = ST_;
     static constexpr bool VEC = VEC_;
@@ -36,6 +36,10 @@ struct DCfg {
     // ping-pong issue: the waves [0, 4) and [4, 8) -- one per SIMD each -- take
     // turns issuing a whole K step; the other half starts its MFMAs at once
     static constexpr bool PP = PP_;
+    // operand moved through VGPRs instead of DMA (its rows need not be 16-byte
+    // aligned): 0 none, 1 A, 2 B
+    static constexpr int VG = VG_;
+    static constexpr bool DMA_A = VG != 1, DMA_B = VG != 2;
     static constexpr bool H = true;
     static constexpr int EB = 2;
     static constexpr int NWAVE = WM * WN, NT = NWAVE * 64;
@@ -44,14 +48,17 @@ struct DCfg {
     static constexpr int ACC = MI == 16 ? 4 : 16;
     static constexpr int KI = MI == 16 ? 32 : 16;
     static constexpr int A_BYTES = MB * KB * 2, B_BYTES = KB * NB * 2;
+    static constexpr int CPA_ = KB / 8, CPB_ = NB / 8;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
     static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;   // the whole ring
     static constexpr int CPA = KB / 8, CPB = NB / 8;       // 16-byte chunks per row
     static constexpr int SWA = CPA < 16 ? CPA : 16;        // A swizzle period (rows)
     static constexpr int LANE_BYTES = 16;                  // bytes one lane moves per DMA instruction
     static constexpr int WAVE_BYTES = 64 * LANE_BYTES;
-    static constexpr int A_IPW = A_BYTES / WAVE_BYTES / NWAVE;   // DMA instructions per wave per K step
-    static constexpr int B_IPW = B_BYTES / WAVE_BYTES / NWAVE;
+    static constexpr int A_IPW = DMA_A ? A_BYTES / WAVE_BYTES / NWAVE : 0;   // DMA instructions per wave per K step
+    static constexpr int B_IPW = DMA_B ? B_BYTES / WAVE_BYTES / NWAVE : 0;
+    // 16-byte chunks per thread of the operand moved through VGPRs
+    static constexpr int VGC = VG == 1 ? MB * CPA_ / NT : VG == 2 ? KB * CPB_ / NT : 0;
     static constexpr int LPS = A_IPW + B_IPW;
 
     // With a ring of 3 or more stages the next K step's DMA is spread between
@@ -65,8 +72,10 @@ struct DCfg {
     static_assert(VEC, "direct-to-LDS loads move 16-byte chunks");
     static_assert(MB % WM == 0 && NB % WN == 0 && MW % MI == 0 && NW % MI == 0, "tile hierarchy");
     static_assert(KB % KI == 0 && KB % 8 == 0 && NB % 8 == 0, "K step and chunking");
-    static_assert(A_IPW >= 1 && A_IPW * WAVE_BYTES * NWAVE == A_BYTES, "A DMA must split evenly over waves");
-    static_assert(B_IPW >= 1 && B_IPW * WAVE_BYTES * NWAVE == B_BYTES, "B DMA must split evenly over waves");
+    static_assert(!DMA_A || (A_IPW >= 1 && A_IPW * WAVE_BYTES * NWAVE == A_BYTES), "A DMA must split evenly over waves");
+    static_assert(!DMA_B || (B_IPW >= 1 && B_IPW * WAVE_BYTES * NWAVE == B_BYTES), "B DMA must split evenly over waves");
+    static_assert(VG == 0 || (STAGES == 2 && !CONV && !PP && VGC >= 1 && VGC * NT == (VG == 1 ? MB * CPA : KB * CPB)),
+                  "an operand through VGPRs: 2-stage ring, chunks split evenly over the threads");
     static_assert(STAGES >= 2 && STAGES <= 16, "pipeline depth");
     static_assert((STAGES - 1) * LPS <= 63, "vmcnt range: the prologue's DMA all in flight");
     static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
@@ -222,10 +231,11 @@ struct DmaTile {
     // step can be issued whole (issue) or one instruction at a time (one<I>),
     // so that the main loop can spread it between the MFMAs of the step being
     // computed.
-    static constexpr int A_IPW = C::A_BYTES / C::WAVE_BYTES / NI;
-    static constexpr int B_IPW = C::B_BYTES / C::WAVE_BYTES / NI;
+    static constexpr int A_IPW = C::DMA_A ? C::A_BYTES / C::WAVE_BYTES / NI : 0;
+    static constexpr int B_IPW = C::DMA_B ? C::B_BYTES / C::WAVE_BYTES / NI : 0;
     static constexpr int LPS = A_IPW + B_IPW;
-    static_assert(A_IPW * NI * C::WAVE_BYTES == C::A_BYTES && B_IPW * NI * C::WAVE_BYTES == C::B_BYTES,
+    static_assert((!C::DMA_A || A_IPW * NI * C::WAVE_BYTES == C::A_BYTES) &&
+                      (!C::DMA_B || B_IPW * NI * C::WAVE_BYTES == C::B_BYTES),
                   "the step splits evenly over the issuing waves");
     lds_char* stage;
     u32x4 ra, rb;   // A resource at column k0 of the panel; B resource at row k0, column n0
@@ -293,6 +303,71 @@ struct DmaTile {
     __device__ __forceinline__ void issue(int Mrel, int N, int K, int wave, int lane) const
     {
         range<0, LPS>(Mrel, N, K, wave, lane);
+    }
+};
+
+// The operand of a mixed kernel whose rows need not start on 16-byte
+// boundaries moves through VGPRs: 16-byte row chunks, a chunk wholly inside
+// its row as one (possibly misaligned) load, the chunk that straddles the
+// row's valid end gathered element by element, rows out of range as zeros;
+// then written to the LDS stage at the positions the DMA of an aligned operand
+// would fill, so the fragment reads are the same.
+template <class C>
+struct VgOperand {
+    u32x4 r[C::VGC > 0 ? C::VGC : 1];
+
+    __device__ __forceinline__ static u32x4 gather(const char* p, int valid)
+    {
+        u32x4 x = {0, 0, 0, 0};
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+            const unsigned lo = e < valid ? ((const uint16_t*)p)[e] : 0u;
+            const unsigned hi = e + 1 < valid ? ((const uint16_t*)p)[e + 1] : 0u;
+            x[e >> 1] = pack2(lo, hi);
+        }
+        return x;
+    }
+
+    // the K step at k0: A rows of the panel (VG 1) or B rows k0.. from column n0 (VG 2)
+    __device__ __forceinline__ void load(const char* Apanel, const char* Bbatch, int k0, int kend, int Mrel, int n0,
+                                         int N, int K, int t)
+    {
+#pragma unroll
+        for (int v = 0; v < C::VGC; ++v) {
+            const int idx = t + v * C::NT;
+            u32x4 x = {0, 0, 0, 0};
+            if constexpr (C::VG == 1) {
+                const int rr = idx / C::CPA, gk = k0 + (idx % C::CPA) * 8;
+                if (rr < Mrel && gk < kend) {
+                    const char* p = Apanel + ((int64_t)rr * K + gk) * 2;
+                    x = gk + 8 <= kend ? *(const u32x4_u*)p : gather(p, kend - gk);
+                }
+            } else {
+                const int gk = k0 + idx / C::CPB, gn = n0 + (idx % C::CPB) * 8;
+                if (gk < kend && gn < N) {
+                    const char* p = Bbatch + ((int64_t)gk * N + gn) * 2;
+                    x = gn + 8 <= N ? *(const u32x4_u*)p : gather(p, N - gn);
+                }
+            }
+            r[v] = x;
+        }
+    }
+
+    __device__ __forceinline__ void store(lds_char* stage, int t) const
+    {
+#pragma unroll
+        for (int v = 0; v < C::VGC; ++v) {
+            const int idx = t + v * C::NT;
+            lds_char* dst;
+            if constexpr (C::VG == 1) {
+                const int rr = idx / C::CPA, c = idx % C::CPA;
+                dst = stage + rr * (C::KB * 2) + ((c ^ swz_a(rr, C::SWA)) << 4);
+            } else {
+                const int kk = idx / C::CPB, c = idx % C::CPB;
+                dst = stage + C::A_BYTES + kk * (C::NB * 2) + (b_pos<C::CPB>(c, kk) << 4);
+            }
+            *(lds_u32x4*)dst = r[v];
+        }
     }
 };
 
@@ -437,7 +512,40 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
     for (int s = 0; s < C::STAGES - 1; ++s)
         if (s < g.nk)
             tile(VX_STAGE(s), g.kbeg + s * C::KB).issue(Mrel, p.N, p.K, wave, lane);
-    if constexpr (C::PP) {
+    if constexpr (C::VG != 0) {
+        // Mixed (2 stages): the aligned operand by DMA, the other through VGPRs.
+        // The VGPR loads of step it+1 fly with its DMA while step it computes,
+        // then land in the free stage before the next barrier.
+        VgOperand<C> vg;
+        const DmaTile<C> none(VX_STAGE(0), Apanel, Bbatch, g.kbeg, g.kend, g.n0, p.N);
+        if (g.nk > 0) {
+            vg.load(Apanel, Bbatch, g.kbeg, g.kend, Mrel, g.n0, p.N, p.K, t);
+            wait_vm<0>();
+            vg.store(VX_STAGE(0), t);
+        }
+        for (int it0 = 0; it0 < g.nk; it0 += 2) {
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int it = it0 + j;
+                if (it >= g.nk)
+                    break;
+                wait_vm<0>();        // the DMA of step it has landed
+                __syncthreads();     // ... and every wave's part of it, DMA and LDS writes; stage j ^ 1 is free
+                const bool more = it + 1 < g.nk;
+                if (more) {
+                    const int k1 = g.kbeg + (it + 1) * C::KB;
+                    DmaTile<C>(VX_STAGE(j ^ 1), Apanel, Bbatch, k1, g.kend, g.n0, p.N).issue(Mrel, p.N, p.K, wave, lane);
+                    vg.load(Apanel, Bbatch, k1, g.kend, Mrel, g.n0, p.N, p.K, t);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, none, false, Mrel, p.N, p.K, wave);
+                if (more) {
+                    wait_vm<0>();
+                    vg.store(VX_STAGE(j ^ 1), t);
+                }
+            }
+        }
+    } else if constexpr (C::PP) {
         // Ping-pong (2 stages): step 0 came from every wave above; then at
         // step it the half (wave >> 2) == it % 2 issues step it+1 whole into
         // the other stage while the other half starts its MFMAs right after

@@ -80,7 +80,7 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
     const bool hyb = split < 0;
     if (hyb)
         split = -split;
-    if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || split < 1 || k.op != sh.op)
+    if (!k.enabled || (int)k.dtype != sh.dt || (k.align & ~sh.vec_ok) || split < 1 || k.op != sh.op)
         return -1.0;
     if (hyb && (split < 2 || sh.K == 0))
         return -1.0;
@@ -199,7 +199,7 @@ double vxi_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k,
         // straddle an extra cache line per row segment and the ragged edge chunks
         // are gathered element by element
         const double bw_wg = bw_wg_at(pc);
-        const double load_factor = k.vec ? 1.0 : 1.25;
+        const double load_factor = k.align == 3 ? 1.0 : k.align == 0 ? 1.25 : 1.12;
         // (family 2 reads only B from memory in the loop; its A slice is loaded once)
         const double xfer = (double)(valu ? k.nb : k.mb + k.nb) * k.kb * eb * load_factor / bw_wg;
         const double t_load = hw.mem_latency_ns + xfer;
@@ -240,7 +240,7 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
             continue;
         if (!(f.backends & (k.family == 2 ? 2 : 1)))
             continue;
-        if (!k.enabled || (int)k.dtype != sh.dt || (k.vec && !sh.vec_ok) || k.op != sh.op)
+        if (!k.enabled || (int)k.dtype != sh.dt || (k.align & ~sh.vec_ok) || k.op != sh.op)
             continue;   // infeasible at every split (the same test opens vxi_cost)
         // (split, hybrid grid) pairs: each split plain, then (split >= 2) hybrid
         int pairs[2 * (int)(sizeof(kSplits) / sizeof(kSplits[0]))][2];

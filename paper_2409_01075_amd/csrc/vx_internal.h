@@ -37,7 +37,7 @@ int vxi_device_hwinfo(int device, vx_hwinfo* out);
 struct VxShape {
     int64_t batch, M, N, K;
     int dt;        // vx_dtype
-    int vec_ok;    // operands allow 16-byte vector loads
+    int vec_ok;    // rows allow 16-byte vector loads: bit 0 A's, bit 1 B's (3: both)
     int c_vec;     // C allows 4-element vector stores
     int op = 0;    // 0: GEMM; 1: 2-D convolution as an implicit GEMM (conv kernels only)
     int64_t a_bytes = 0;   // convolution: bytes of the image (the direct-to-LDS kernels need < 2^31)

@@ -30,7 +30,7 @@ class vx_kernel_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in (
         "id", "dtype", "mb", "nb", "kb", "wm", "wn", "mfma_m", "mfma_n", "mfma_k", "vec", "family", "stages",
         "threads",
-        "lds_bytes", "vgprs", "agprs", "sgprs", "scratch_bytes", "enabled", "k_max", "op", "schedule")]
+        "lds_bytes", "vgprs", "agprs", "sgprs", "scratch_bytes", "enabled", "k_max", "op", "align", "schedule")]
 
 
 class vx_conv2d_desc(ctypes.Structure):
@@ -145,9 +145,9 @@ def vx_plan_query(batch, M, N, K, dtype, sA=None, sB=None, sC=None, base_align=2
     return p
 
 
-def vx_plan_cost(batch, M, N, K, dtype, kernel_id, split_k, vec_ok=1):
+def vx_plan_cost(batch, M, N, K, dtype, kernel_id, split_k, align=3):
     c = ctypes.c_double()
-    st = lib().vx_plan_cost(batch, M, N, K, dtype, kernel_id, split_k, vec_ok, ctypes.byref(c))
+    st = lib().vx_plan_cost(batch, M, N, K, dtype, kernel_id, split_k, align, ctypes.byref(c))
     return st, c.value
 
 

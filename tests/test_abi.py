@@ -74,7 +74,7 @@ def test_calibration_file_rules(tmp_path):
         p_cal = vx.vx_plan_query(1, 4096, 4096, 4096, 1)
         assert (p_cal.kernel.mb, p_cal.kernel.nb, p_cal.kernel.kb) == (64, 64, 64)
         # the argmin still holds against the model it uses
-        st, c = vx.vx_plan_cost(1, 4096, 4096, 4096, 1, p_cal.kernel_id, p_cal.split_k, 1)
+        st, c = vx.vx_plan_cost(1, 4096, 4096, 4096, 1, p_cal.kernel_id, p_cal.split_k, 3)
         assert st == 0 and c == pytest.approx(p_cal.predicted_ns)
         vx.vx_calibration_enable(False)
         assert vx.vx_calibration_active() == 0
@@ -177,6 +177,9 @@ def test_registry_invariants():
         assert k.lds_bytes <= 160 * 1024
         assert k.enabled == (1 if k.scratch_bytes == 0 else 0)
         assert k.vgprs + k.agprs <= 512 and k.vgprs > 0
+        assert k.vec == (1 if k.align == 3 else 0)
+        if k.family == 1:
+            assert k.align in (1, 2, 3)        # at least one operand moves by DMA
         seen.add((k.dtype, k.vec))
     assert seen == {(d, v) for d in (0, 1, 2) for v in (0, 1)}
     assert valu > 0
@@ -233,11 +236,13 @@ def test_selector_plans_cover_and_are_feasible(mi355x_override):
                 p = vx.vx_plan_query(b, M, N, K, dt, base_align=align)
                 k = p.kernel
                 assert k.enabled and k.dtype == dt
+                ve = 8 if dt else 4
                 if align == 2:
-                    assert k.vec == 0
-                if k.vec:
-                    ve = 8 if dt else 4
-                    assert K % ve == 0 and N % ve == 0
+                    assert k.align == 0 and k.vec == 0
+                if k.align & 1:
+                    assert K % ve == 0
+                if k.align & 2:
+                    assert N % ve == 0
                 assert p.tiles_m * k.mb >= M and (p.tiles_m - 1) * k.mb < M
                 assert p.tiles_n * k.nb >= N and (p.tiles_n - 1) * k.nb < N
                 tiles = p.tiles_m * p.tiles_n * b
@@ -273,7 +278,7 @@ def test_selector_is_the_argmin_of_the_cost_model(mi355x_override):
                              (2, (192, 333, 333, 64)), (2, (192, 336, 336, 64)), (0, (1, 77, 96, 80)), (2, (1, 16, 11008, 4096))]:
         p = vx.vx_plan_query(b, M, N, K, dt)
         ve = 8 if dt else 4
-        vec_ok = int(K % ve == 0 and N % ve == 0)
+        vec_ok = int(K % ve == 0 and (b == 1 or M * K % ve == 0)) | 2 * int(N % ve == 0 and (b == 1 or K * N % ve == 0))
         best = min(c for i in range(n) for s in splits
                    for st, c in [vx.vx_plan_cost(b, M, N, K, dt, i, s, vec_ok)] if st == 0)
         assert p.predicted_ns == pytest.approx(best, rel=1e-12)
@@ -321,7 +326,7 @@ def test_fix_wavefront_restricts_the_argmin(mi355x_override):
             assert wave(p.kernel) == strat
             assert p.predicted_ns >= p0.predicted_ns
             best = min(c for k in reg if k.enabled and k.dtype == dt and wave(k) == strat for s in splits
-                       for st, c in [vx.vx_plan_cost(b, M, N, K, dt, k.id, s, 1)] if st == 0)
+                       for st, c in [vx.vx_plan_cost(b, M, N, K, dt, k.id, s, 3)] if st == 0)
             assert p.predicted_ns == pytest.approx(best, rel=1e-12)
             assert vx.vx_fix_wavefront(0, 0, 0) == 0
             p1 = vx.vx_plan_query(b, M, N, K, dt)
@@ -435,7 +440,7 @@ def test_hybrid_grid_plans(mi355x_override):
         if k.op or k.dtype != dt or not k.enabled:
             continue
         tiles = -(-M // k.mb) * -(-N // k.nb)
-        st, c = vx.vx_plan_cost(b, M, N, K, dt, k.id, -2, 1)
+        st, c = vx.vx_plan_cost(b, M, N, K, dt, k.id, -2, 3)
         if tiles <= slots(k.id) or tiles % slots(k.id) == 0:
             assert st == 3, (k.id, tiles)
         elif st == 0:

@@ -146,8 +146,8 @@ def _kernel_cases():
 def _shape_for(k, extra_m=3, extra_n=5, extra_k=8):
     """A ragged shape spanning 2 x 2 tiles and a K tail for kernel k."""
     M = 2 * k.mb + extra_m
-    N = k.nb + (8 if k.vec else extra_n)
-    K = 2 * k.kb + (8 if k.vec else extra_k + 1)
+    N = k.nb + (8 if k.align & 2 else extra_n)           # B's rows aligned only where the kernel needs it
+    K = 2 * k.kb + (8 if k.align & 1 else extra_k + 1)   # likewise A's
     return M, N, K
 
 
@@ -225,7 +225,7 @@ def test_split_k_integer_exact(code, split):
     picked = [k for k in _kernel_cases() if k.dtype == code and k.enabled][::7]
     for k in picked:
         M, N, _ = _shape_for(k)
-        K = split * k.kb + (8 if k.vec else 5)
+        K = split * k.kb + (8 if k.align & 1 else 5)
         r = max(1, min(4, I.exact_range(K, code)))
         A = I.small_int(g, (M, K), code, -r, r)
         B = I.small_int(g, (K, N), code, -r, r)
@@ -274,7 +274,7 @@ def test_guard_bands_and_canaries(code):
         Bt = to_dev(Bg.view(np.float32) if code == 0 else Bg, code)
         Ct = empty_out((M * N + 2 * pad,), code, fill_bits=0x5a5a)
         for sp in (1, 3):
-            ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and not k.vec]
+            ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and k.align == 0]
             for k in [None] + ks[::13]:
                 vx.vx_force_plan(-1 if k is None else k.id, sp)
                 st = vx.vx_gemm(M, N, K, code, At.data_ptr() + pad * At.element_size(),
@@ -319,7 +319,7 @@ def _hybrid_shape(k, code):
     tiles_n = max(2, min(16, target // 8))
     tiles_m = -(-target // tiles_n)
     M = tiles_m * k.mb - 3
-    N = tiles_n * k.nb - (8 if k.vec else 5)
+    N = tiles_n * k.nb - (8 if k.align & 2 else 5)
     return M, N, tiles_m * tiles_n
 
 
@@ -345,12 +345,12 @@ def test_hybrid_grid_integer_exact(code):
     ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled]
     picked = {}
     for k in ks:
-        picked.setdefault((k.family, k.vec, k.mb * k.nb >= 128 * 128), k)
+        picked.setdefault((k.family, k.align, k.mb * k.nb >= 128 * 128), k)
     ran = 0
     for k in picked.values():
         M, N, tiles = _hybrid_shape(k, code)
         for split in (2, 3):
-            K = 2 * split * k.kb + (8 if k.vec else 5)
+            K = 2 * split * k.kb + (8 if k.align & 1 else 5)
             if k.k_max and K > k.k_max:
                 continue
             r = max(1, min(3, I.exact_range(K, code)))
@@ -382,7 +382,7 @@ def test_hybrid_grid_random_within_bound(code):
     A = I.normal(g, (M, K), code)
     B = I.normal(g, (K, N), code, 0.02)
     ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and k.vec and k.mb == 128 and k.nb == 128
-          and vx.vx_plan_cost(1, M, N, K, code, k.id, -3, 1)[0] == 0]
+          and vx.vx_plan_cost(1, M, N, K, code, k.id, -3, 3)[0] == 0]
     assert ks
     k = ks[0]
     assert vx.vx_force_plan(k.id, -3) == 0
@@ -395,3 +395,43 @@ def test_hybrid_grid_random_within_bound(code):
     rows, cols = _tile_samples(g, M, N, k.mb, k.nb)
     ref, mag = oracle.gemm_sampled(A, B, code, M, N, K, rows, cols)
     tolerance.check(C[rows, cols], ref, mag, code, "hybrid kernel %d" % k.id)
+
+
+@pytest.mark.parametrize("code", [1, 2])
+def test_mixed_kernels_guard_bands(code):
+    """Every mixed kernel (one operand by DMA, the one with unaligned rows
+    through VGPRs) on a ragged shape whose other operand is unaligned, inside
+    NaN guard bands (an out-of-bounds read would leak NaN into C) with
+    canaries around C, random values within the bound."""
+    import torch
+    from .gpu_util import to_dev, empty_out
+    g = I.rng(980 + code)
+    nan = 0x7fc0
+    pad = 4096
+    ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and k.family == 1 and k.align in (1, 2)]
+    assert ks
+    for k in ks:
+        M = 2 * k.mb + 3
+        N = k.nb + (8 if k.align & 2 else 5)
+        K = 2 * k.kb + (8 if k.align & 1 else 11)
+        A = I.normal(g, (M, K), code)
+        B = I.normal(g, (K, N), code)
+        Ag = np.full(M * K + 2 * pad, nan, dtype=np.uint16)
+        Ag[pad:pad + M * K] = A.reshape(-1).view(np.uint16)
+        Bg = np.full(K * N + 2 * pad, nan, dtype=np.uint16)
+        Bg[pad:pad + K * N] = B.reshape(-1).view(np.uint16)
+        At, Bt = to_dev(Ag, code), to_dev(Bg, code)
+        Ct = empty_out((M * N + 2 * pad,), code, fill_bits=0x5a5a)
+        assert vx.vx_force_plan(k.id, 1) == 0
+        try:
+            st = vx.vx_gemm(M, N, K, code, At.data_ptr() + 2 * pad, Bt.data_ptr() + 2 * pad, Ct.data_ptr() + 2 * pad,
+                            torch.cuda.current_stream().cuda_stream)
+        finally:
+            vx.vx_force_plan(-1, 0)
+        assert st == 0, (k.id, vx.STATUS.get(st, st))
+        torch.cuda.synchronize()
+        out = from_dev(Ct, code)
+        assert np.all(out[:pad] == 0x5a5a) and np.all(out[pad + M * N:] == 0x5a5a), k.id
+        ref, mag = oracle.gemm(A, B, code)
+        tolerance.check(out[pad:pad + M * N].reshape(M, N), ref, mag, code,
+                        "mixed kernel %d align %d %s" % (k.id, k.align, (M, N, K)))
