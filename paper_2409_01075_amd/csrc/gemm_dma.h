@@ -5,10 +5,14 @@
 // so up to STAGES-1 K steps are in flight while the MFMAs consume the oldest.
 // Out-of-range rows, columns and K tails are given an out-of-range buffer
 // offset: the hardware returns zeros for them, which land in LDS as padding.
-// Each lane moves one 16-byte chunk, so rows must be 16-byte aligned (K and N
-// multiples of 8, aligned bases); other operands use the register-staged
+// Each lane moves one 16-byte chunk, so a DMA'd operand's rows must be 16-byte
+// aligned (K for A, N for B a multiple of 8, aligned bases).  Mixed kernels
+// (VG) move one operand whose rows are not aligned through VGPRs into the same
+// LDS layout; GEMMs with neither operand aligned use the register-staged
 // family (a 2-byte buffer-to-LDS load fills a whole LDS dword per lane, which
-// cannot build a dense 16-bit tile).
+// cannot build a dense 16-bit tile).  Three level-1 schedules: the plain ring
+// (every wave issues its share of each K step), ping-pong (PP: the two halves
+// of the waves take turns issuing whole K steps) and mixed (VG).
 //
 // LDS layouts (dense, 16-byte chunks XOR-swizzled against bank conflicts):
 //   As[m][k]  Mb x Kb, k contiguous   (chunk c of row m stored at c ^ swzA(m))
