@@ -60,6 +60,9 @@ def _parse():
                          "ablations, with the best")
     ap.add_argument("--no-hybrid", action="store_true",
                     help="ablation: the selector does not consider the hybrid grid")
+    ap.add_argument("--no-krot", action="store_true",
+                    help="ablation: the direct-to-LDS GEMM kernels walk each tile's K steps in order "
+                         "instead of from a per-tile rotated start")
     ap.add_argument("--no-calibration", action="store_true",
                     help="ablation: plan with the purely analytical cost model (ignore the calibration table)")
     ap.add_argument("--compare-torch", action="store_true",
@@ -118,9 +121,13 @@ def _copy_calibration(args, dev):
     del src, dst
 
 
+_ABLATIONS = []   # ablation switches given on the command line
+
+
 def _selector_kind():
     from paper_2409_01075_amd import vx
-    return "hybrid (calibrated)" if vx.vx_calibration_active() else "analytical"
+    kind = "hybrid (calibrated)" if vx.vx_calibration_active() else "analytical"
+    return kind + ("; ablations: " + ", ".join(_ABLATIONS) if _ABLATIONS else "")
 
 
 def _cpu_threads():
@@ -751,6 +758,11 @@ def main():
     if args.no_hybrid:
         from paper_2409_01075_amd import vx
         vx.vx_enable_hybrid_grid(0)
+        _ABLATIONS.append("no-hybrid")
+    if args.no_krot:
+        from paper_2409_01075_amd import vx
+        vx.vx_enable_k_rotation(0)
+        _ABLATIONS.append("no-krot")
     if args.study:
         run_study(args)
         return

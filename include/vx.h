@@ -250,6 +250,21 @@ vx_status vx_restrict_backends(int mask);
 vx_status vx_enable_hybrid_grid(int enable);
 
 /*
+ * Workgroup-level ablation of the rotated K order.  With enable = 1 (the
+ * default), a GEMM whose A and B of one batch entry together fit in one XCD's
+ * L2 (vx_hwinfo.l2_bytes_per_xcd), run by a plain-ring direct-to-LDS kernel
+ * (vx_kernel_info.family 1, schedule 0), starts tile (tm, tn) at step
+ * (tm + tn) mod nk of its K slice and wraps around, so that the tiles sharing
+ * an A or B panel do not request the same L2 lines at the same time.  Every
+ * other call, and every call with enable = 0, walks K in order.  Either way
+ * each output element is the fp32 sum of the same products; only the order of
+ * that sum differs (fixed per tile, so repeated calls stay bit-identical).
+ * Takes effect at the next launch; plans are unaffected.  Process-wide; for
+ * studies and tests.
+ */
+vx_status vx_enable_k_rotation(int enable);
+
+/*
  * Hand the library a caller-owned device buffer to use as the split-K
  * workspace of `stream` (NULL/0 bytes: return to the library's own lazily
  * allocated buffer).  The buffer must stay valid until the stream's work

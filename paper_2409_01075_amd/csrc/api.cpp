@@ -37,6 +37,7 @@ std::atomic<int> g_force_split{0};
 std::atomic<int> g_fix_wm{0}, g_fix_wn{0}, g_fix_mi{0};
 std::atomic<int> g_backends{3};   // kernel backends the selector may use (vx_restrict_backends)
 std::atomic<bool> g_hybrid{true};  // hybrid grids among the plans (vx_enable_hybrid_grid)
+std::atomic<bool> g_krot{true};    // rotated K order in the direct-to-LDS GEMM kernels (vx_enable_k_rotation)
 std::atomic<uint64_t> g_epoch{0};   // bumps when planning inputs change
 
 struct PlanKey {
@@ -374,6 +375,9 @@ vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream)
     a.num_xcd = hw.num_xcd;
     a.grid = (int)plan.grid;
     a.dp_tiles = (int)plan.dp_tiles;
+    // rotated K order where one batch entry's operands stay resident in an
+    // XCD's L2 (the plain-ring direct-to-LDS kernels read it)
+    a.krot = g_krot.load() && (double)(sh.M * sh.K + sh.K * sh.N) * elem_bytes(sh.dt) <= hw.l2_bytes_per_xcd ? 1 : 0;
     a.ws = plan.split_k > 1 ? (float*)(ws.base + kTicketBytes) : nullptr;
     a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
     hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);
@@ -711,6 +715,13 @@ vx_status vx_enable_hybrid_grid(int enable)
     g_hybrid.store(enable != 0);
     g_plans.clear();
     g_epoch.fetch_add(1);
+    return VX_OK;
+}
+
+vx_status vx_enable_k_rotation(int enable)
+{
+    // launch-time only: plans do not depend on it
+    g_krot.store(enable != 0);
     return VX_OK;
 }
 

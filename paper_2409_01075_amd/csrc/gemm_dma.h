@@ -14,6 +14,17 @@
 // (every wave issues its share of each K step), ping-pong (PP: the two halves
 // of the waves take turns issuing whole K steps) and mixed (VG).
 //
+// K order (plain ring, GEMM only; the host sets krot when one batch entry's A
+// and B fit in an XCD's L2): a tile takes its slice's K steps starting at step
+// (tm + tn) mod nk, wrapping around.  The tiles resident at one time on an XCD
+// share A row panels and B column panels; walked in lockstep, every one of them
+// asks the L2 for the same lines at the same moment.  With the operands
+// resident, rotating the start spreads those requests over the panels' K
+// extent.  Larger operands stream through the L2, and there the lockstep is
+// what lets one tile's miss serve its neighbours, so they keep the in-order
+// walk.  Only the order of the fp32 accumulation changes, and it is a fixed
+// function of the tile.
+//
 // LDS layouts (dense, 16-byte chunks XOR-swizzled against bank conflicts):
 //   As[m][k]  Mb x Kb, k contiguous   (chunk c of row m stored at c ^ swzA(m))
 //   Bs[k][n]  Kb x Nb, n contiguous   (chunk c of row k stored at c ^ swzB(k);
@@ -471,7 +482,8 @@ __device__ __forceinline__ void dma_compute(lds_char* stage, Acc<C>& acc, int wm
 template <class C>
 __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
 {
-    VxGemmArgs p = pin_args(args);
+    constexpr bool KROT = !C::CONV && !C::PP && C::VG == 0;   // kernels that may rotate their K order
+    VxGemmArgs p = pin_args<KROT>(args);
     if constexpr (C::CONV)
         pin_conv(p);
     // The ring: STAGES stages of one K step each.  Stage indices are
@@ -512,10 +524,27 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
             return DmaTile<C>(st, Apanel, Bbatch, k0, g.kend, g.n0, p.N);
         }
     };
+    int rot = 0;
+    if constexpr (KROT)
+        rot = p.krot != 0 && g.nk > 1 ? (g.tm + g.tn) % g.nk : 0;
+    // K offset of the step the tile takes s-th: in order, or rotated by rot
+    // (rc is std::true_type); a step s >= nk is never issued, any offset does
+    auto kstep = [&](auto rc, int s) {
+        if constexpr (decltype(rc)::value) {
+            const int q = s + rot;
+            return g.kbeg + (q >= g.nk ? q - g.nk : q) * C::KB;
+        } else {
+            return g.kbeg + s * C::KB;
+        }
+    };
+    auto prologue = [&](auto rc) {
 #pragma unroll
-    for (int s = 0; s < C::STAGES - 1; ++s)
-        if (s < g.nk)
-            tile(VX_STAGE(s), g.kbeg + s * C::KB).issue(Mrel, p.N, p.K, wave, lane);
+        for (int s = 0; s < C::STAGES - 1; ++s)
+            if (s < g.nk)
+                tile(VX_STAGE(s), kstep(rc, s)).issue(Mrel, p.N, p.K, wave, lane);
+    };
+    if constexpr (C::VG != 0 || C::PP)
+        prologue(std::false_type{});
     if constexpr (C::VG != 0) {
         // Mixed (2 stages): the aligned operand by DMA, the other through VGPRs.
         // The VGPR loads of step it+1 fly with its DMA while step it computes,
@@ -572,21 +601,35 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
             }
         }
     } else {
-        // main loop, unrolled by STAGES so that every stage index is a constant
-        for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
+        // the plain ring: prologue, then the main loop, unrolled by STAGES so
+        // that every stage index is a constant.  The rotated and the in-order
+        // walks are separate instances, so the in-order one carries no
+        // rotation arithmetic.
+        auto ring = [&](auto rc) {
+            prologue(rc);
+            for (int it0 = 0; it0 < g.nk; it0 += C::STAGES) {
 #pragma unroll
-            for (int j = 0; j < C::STAGES; ++j) {
-                const int it = it0 + j;
-                if (it >= g.nk)
-                    break;
-                wait_steps<C::LPS, C::STAGES - 2>(g.nk - 1 - it);   // step `it` has landed (this wave's part)
-                __builtin_amdgcn_s_barrier();                      // ... and every wave's; stage it-1 is free
-                // step it+STAGES-1 goes into the freed stage, issued between the MFMAs of step it
-                const DmaTile<C> next =
-                    tile(VX_STAGE((j + C::STAGES - 1) % C::STAGES), g.kbeg + (it + C::STAGES - 1) * C::KB);
-                dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, next, it + C::STAGES - 1 < g.nk, Mrel, p.N, p.K,
-                               wave);
+                for (int j = 0; j < C::STAGES; ++j) {
+                    const int it = it0 + j;
+                    if (it >= g.nk)
+                        break;
+                    wait_steps<C::LPS, C::STAGES - 2>(g.nk - 1 - it);   // step `it` has landed (this wave's part)
+                    __builtin_amdgcn_s_barrier();                      // ... and every wave's; stage it-1 is free
+                    // step it+STAGES-1 goes into the freed stage, issued between the MFMAs of step it
+                    const DmaTile<C> next =
+                        tile(VX_STAGE((j + C::STAGES - 1) % C::STAGES), kstep(rc, it + C::STAGES - 1));
+                    dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, next, it + C::STAGES - 1 < g.nk, Mrel, p.N,
+                                   p.K, wave);
+                }
             }
+        };
+        if constexpr (KROT) {
+            if (rot != 0)
+                ring(std::true_type{});
+            else
+                ring(std::false_type{});
+        } else {
+            ring(std::false_type{});
         }
     }
     wait_vm<0>();   // nothing is in flight here; kept as a guard before LDS is released

@@ -470,13 +470,21 @@ __device__ __forceinline__ void acc_coord(int lane, int g, int& dm, int& dn)
 // start, so every batch costs a memory round trip before the first operand
 // load can be issued.  Pinning every field at entry issues all the loads
 // together and waits once.
+// KROT: the kernel also reads krot.
+template <bool KROT = false>
 __device__ __forceinline__ VxGemmArgs pin_args(const VxGemmArgs& in)
 {
     VxGemmArgs p = in;
-    asm volatile("" : "+s"(p.A), "+s"(p.B), "+s"(p.C), "+s"(p.sA), "+s"(p.sB), "+s"(p.sC), "+s"(p.M), "+s"(p.N),
-                      "+s"(p.K), "+s"(p.tiles_m), "+s"(p.tiles_n), "+s"(p.split), "+s"(p.k_per_split),
-                      "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.dp_tiles), "+s"(p.ws),
-                      "+s"(p.tickets));
+    if constexpr (KROT)
+        asm volatile("" : "+s"(p.A), "+s"(p.B), "+s"(p.C), "+s"(p.sA), "+s"(p.sB), "+s"(p.sC), "+s"(p.M), "+s"(p.N),
+                          "+s"(p.K), "+s"(p.tiles_m), "+s"(p.tiles_n), "+s"(p.split), "+s"(p.k_per_split),
+                          "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.dp_tiles),
+                          "+s"(p.ws), "+s"(p.tickets), "+s"(p.krot));
+    else
+        asm volatile("" : "+s"(p.A), "+s"(p.B), "+s"(p.C), "+s"(p.sA), "+s"(p.sB), "+s"(p.sC), "+s"(p.M), "+s"(p.N),
+                          "+s"(p.K), "+s"(p.tiles_m), "+s"(p.tiles_n), "+s"(p.split), "+s"(p.k_per_split),
+                          "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.dp_tiles),
+                          "+s"(p.ws), "+s"(p.tickets));
     return p;
 }
 

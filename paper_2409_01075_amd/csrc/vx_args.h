@@ -26,4 +26,6 @@ struct VxGemmArgs {
     // K = KH*KW*Cin, B is the filter (KH*KW*Cin x Cout), C the output.
     int cH, cW, cC, cKW, cOH, cOW;
     int csh, csw, cph, cpw, cdh, cdw;   // stride, padding, dilation (height, width)
+    int krot;               // 1: each tile walks its K steps starting at step (tm + tn) mod nk
+                            // (plain-ring direct-to-LDS GEMM kernels); 0: in order
 };

@@ -93,6 +93,8 @@ def lib():
     L.vx_registry_get.restype = i32
     L.vx_enable_hybrid_grid.argtypes = [i32]
     L.vx_enable_hybrid_grid.restype = i32
+    L.vx_enable_k_rotation.argtypes = [i32]
+    L.vx_enable_k_rotation.restype = i32
     L.vx_force_plan.argtypes = [i32, i32]
     L.vx_force_plan.restype = i32
     L.vx_fix_wavefront.argtypes = [i32, i32, i32]
@@ -211,6 +213,10 @@ def vx_restrict_backends(mask=0):
 
 def vx_enable_hybrid_grid(enable=1):
     return lib().vx_enable_hybrid_grid(enable)
+
+
+def vx_enable_k_rotation(enable=1):
+    return lib().vx_enable_k_rotation(enable)
 
 
 def vx_set_workspace(ptr, nbytes, stream=None):

@@ -435,3 +435,84 @@ def test_mixed_kernels_guard_bands(code):
         ref, mag = oracle.gemm(A, B, code)
         tolerance.check(out[pad:pad + M * N].reshape(M, N), ref, mag, code,
                         "mixed kernel %d align %d %s" % (k.id, k.align, (M, N, K)))
+
+
+def _spread(ks, n):
+    """Up to n kernels spread evenly over the list."""
+    if len(ks) <= n:
+        return ks
+    return [ks[(i * (len(ks) - 1)) // (n - 1)] for i in range(n)]
+
+
+@pytest.mark.parametrize("code", [1, 2])
+def test_k_rotation_integer_exact_and_order_only(code):
+    """Direct-to-LDS kernels of each schedule (plain ring, ping-pong, mixed)
+    on a 3 x 3-tile shape whose K slice spans several steps and ends inside
+    one, with the rotation switch on (the default; these operands fit in an
+    XCD's L2, so the plain-ring kernels rotate their K order) and off, unsplit,
+    split 3 and on a hybrid grid where the kernel has one.  Small-integer
+    inputs make every sum exact, so both orders must equal the oracle bit for
+    bit; repeated calls with the rotation must be bit-identical."""
+    g = I.rng(1010 + code)
+    ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and k.family == 1]
+    groups = [[k for k in ks if k.schedule == 0 and k.align == 3], [k for k in ks if k.schedule == 1],
+              [k for k in ks if k.align != 3]]
+    assert all(groups), [len(x) for x in groups]
+    ran = 0
+    try:
+        for grp in groups:
+            for k in _spread(grp, 6):
+                M = 3 * k.mb - 5
+                N = 3 * k.nb - (8 if k.align & 2 else 3)
+                K = 5 * k.kb + (8 if k.align & 1 else 9)
+                r = max(1, min(3, I.exact_range(K, code)))
+                A = I.small_int(g, (M, K), code, -r, r)
+                B = I.small_int(g, (K, N), code, -r, r)
+                ref = oracle.gemm(A, B, code, with_mag=False)
+                for split in (1, 3, -2):
+                    if vx.vx_plan_cost(1, M, N, K, code, k.id, split, k.align)[0] != 0:
+                        continue   # no such plan for this kernel and shape (e.g. no hybrid split)
+                    outs = []
+                    for rot in (1, 0, 1):
+                        assert vx.vx_enable_k_rotation(rot) == 0
+                        assert vx.vx_force_plan(k.id, split) == 0
+                        try:
+                            C = run_gemm(A, B, code)
+                        finally:
+                            vx.vx_force_plan(-1, 0)
+                        tolerance.check_exact(C, ref, code, "kernel %d sched %d align %d split %d rot %d %s" % (
+                            k.id, k.schedule, k.align, split, rot, (M, N, K)))
+                        outs.append(C)
+                    assert np.array_equal(outs[0], outs[2]), k.id
+                    ran += 1
+    finally:
+        vx.vx_enable_k_rotation(1)
+    assert ran >= 12
+
+
+@pytest.mark.parametrize("code", [1, 2])
+def test_k_rotation_random_within_bound(code):
+    """Random operands through rotated and in-order K on the same plans: both
+    within the bound of the oracle, and the two results close to each other
+    (they differ only in the fp32 summation order)."""
+    g = I.rng(1030 + code)
+    ks = [k for k in _kernel_cases() if k.dtype == code and k.enabled and k.family == 1 and k.align == 3]
+    try:
+        for k in _spread(ks, 8):
+            M, N, K = 2 * k.mb + 7, 2 * k.nb + 8, 4 * k.kb + 24
+            A = I.normal(g, (M, K), code)
+            B = I.normal(g, (K, N), code, 0.02)
+            ref, mag = oracle.gemm(A, B, code)
+            res = []
+            for rot in (1, 0):
+                assert vx.vx_enable_k_rotation(rot) == 0
+                assert vx.vx_force_plan(k.id, 1) == 0
+                try:
+                    C = run_gemm(A, B, code)
+                finally:
+                    vx.vx_force_plan(-1, 0)
+                tolerance.check(C, ref, mag, code, "kernel %d rot %d" % (k.id, rot))
+                res.append(oracle.decode(C, code).astype(np.float64))
+            assert np.all(np.abs(res[0] - res[1]) <= 8e-3 * mag + 1e-6), k.id
+    finally:
+        vx.vx_enable_k_rotation(1)
