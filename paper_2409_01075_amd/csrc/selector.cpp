@@ -268,7 +268,11 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
             const double c = vxi_cost(hw, sh, k, pairs[j][1] ? -split : split, lim, &kps, &dp);
             if (c < 0.0)
                 continue;
-            if (c < best) {   // strict: ties keep the earlier (lower id, smaller split, plain grid) candidate
+            // equal predicted costs (plans bounded by the same term, e.g. the
+            // operands' HBM time) go to the fewer K slices: no split-K epilogue
+            // and no partial-tile traffic, which the bound does not see.
+            // Remaining ties keep the earlier (lower id, plain grid) candidate.
+            if (c < best || (c == best && split < best_split)) {
                 best = c;
                 best_id = i;
                 best_split = split;
