@@ -157,6 +157,8 @@ vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype
 /*
  * The cost model's estimate (ns) for running a given kernel with a given
  * split-K factor on a shape; VX_ERR_NO_CANDIDATE if the pair is infeasible.
+ * It is the selector's model: like a plan query, the first call loads the
+ * shipped calibration table when it matches the compiled kernel set.
  * split_k < 0 prices the hybrid grid with -split_k slices per split tile.
  * align: which operands' rows start on 16-byte boundaries (bit 0 A, bit 1 B;
  * 3 both, 0 neither); VX_ERR_INVALID_ARG outside 0..3.

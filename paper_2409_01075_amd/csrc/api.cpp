@@ -627,6 +627,7 @@ vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype 
         return st;
     if (align < 0 || align > 3)
         return VX_ERR_INVALID_ARG;
+    ensure_calib(hw);   // the same model as the selector's, from the first call on
     VxShape sh{batch, M, N, K, (int)dtype, align, 1};
     VxLimits lim{kDefaultPartials, (int64_t)(kTicketBytes / 4)};
     const double c = vxi_cost(hw, sh, reg[kernel_id].info, split_k, lim, nullptr);

@@ -509,3 +509,26 @@ def test_k_rotation_switch_leaves_plans_alone(mi355x_override):
     for p, q in zip(before, after):
         assert (p.kernel_id, p.split_k, p.grid, p.dp_tiles) == (q.kernel_id, q.split_k, q.grid, q.dp_tiles)
         assert p.predicted_ns == q.predicted_ns
+
+
+def test_equal_costs_go_to_fewer_k_slices(mi355x_override):
+    """Among the plans at the minimum predicted cost the selector takes one
+    with the fewest K slices (exact ties occur where the compulsory-bytes floor
+    bounds several plans, e.g. the bf16 decode GEMM (1, 11008, 4096))."""
+    splits = (1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32)
+    reg = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count())) if k.op == 0 and k.enabled]
+    for (M, N, K, dt) in ((1, 11008, 4096, 2), (16, 11008, 4096, 2), (16, 4096, 11008, 2), (1, 4096, 4096, 2),
+                          (300, 768, 768, 1), (77, 96, 80, 0)):
+        p = vx.vx_plan_query(1, M, N, K, dt)   # first, so that the calibration is loaded
+        costs = []
+        for k in reg:
+            if k.dtype != dt:
+                continue
+            for s in splits:
+                for sg in ((s, -s) if s >= 2 else (s,)):
+                    st, c = vx.vx_plan_cost(1, M, N, K, dt, k.id, sg, 3)
+                    if st == 0:
+                        costs.append((c, s))
+        best = min(c for c, _ in costs)
+        fewest = min(s for c, s in costs if c == best)
+        assert p.predicted_ns == best and p.split_k == fewest, ((M, N, K), p.split_k, fewest)
