@@ -297,10 +297,11 @@ def _most_frequent(items):
 def run_study(args):
     """Selector quality and the hierarchy ablations (Section 7.4).
 
-    Pass 1, per GEMM of the set: the time of the selector's plan and of every
-    feasible (kernel, split in {1, 2, 4, 8}, plain grid or hybrid grid for
-    splits 2 and 4) plan of the registry; the best of
-    them stands in for the per-shape profiled upper bound.
+    Pass 1, per GEMM of the set: the time of every feasible (kernel, split in
+    {1, 2, 4, 8}, plain grid or hybrid grid for splits 2 and 4) plan of the
+    registry, one sample each; then the selector's plan and the fastest plans,
+    timed again as a median of 3, until the fastest is a re-timed one.  The
+    best stands in for the per-shape profiled upper bound.
     Pass 2, per dtype and alignment class of the set: Static1 fixes the
     wavefront strategy (wavefront tile and MFMA instruction) that is most
     often optimal over the class's GEMMs and leaves the workgroup tile and the
@@ -324,7 +325,7 @@ def run_study(args):
     spin = int(1e6 / max(e0.elapsed_time(e1), 1e-3) * 0.3)
     reg = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]   # indexed by kernel id
     jobs = _set_jobs(args.workload, args.trials)
-    rows, tables = [], []
+    rows, tables, dones = [], [], []
     vx.vx_force_plan(-1, 0)
     vx.vx_fix_wavefront(0, 0, 0)
     for job in jobs:
@@ -336,7 +337,6 @@ def run_study(args):
         call, R, keep = _study_ctx(job, dev, args.rot_mib, L, sp)
         plan = vx.vx_plan_query(b, M, N, K, dt, M * K, K * N, M * N)
         call(0)
-        t_pick = _time_calls(call, R, stream, spin)
         table = {}
         for k in reg:
             if k.op != 0 or k.dtype != dt or not k.enabled or (k.align & ~vec_ok):
@@ -351,10 +351,32 @@ def run_study(args):
                     table[(k.id, split)] = _time_calls(call, R, stream, spin, reps=1)
                 finally:
                     vx.vx_force_plan(-1, 0)
-        del keep, call
+        # The pass times each plan once; its minimum would be the luckiest of
+        # many noisy samples.  So the selector's pick (through the selector) and
+        # then the pass's fastest plan, until the fastest is one of them, are
+        # timed again like the pick (median of 3, after the pass), and those
+        # times replace the single ones.
         pick = _plan_key(plan)
-        table[pick] = min(t_pick, table.get(pick, t_pick))
-        bk = min(table, key=table.get)
+        done = set()
+
+        def retime(key):
+            if key != pick:
+                vx.vx_force_plan(*key)
+            try:
+                call(0)
+                table[key] = _time_calls(call, R, stream, spin)
+            finally:
+                vx.vx_force_plan(-1, 0)
+            done.add(key)
+        retime(pick)
+        while True:
+            bk = min(table, key=table.get)
+            if bk in done:
+                break
+            retime(bk)
+        del keep, call
+        t_pick = table[pick]
+        dones.append(done)
         kb = reg[bk[0]]
         row = {"label": label, "M": M, "N": N, "K": K, "batch": b, "dtype": dt, "vec_ok": vec_ok,
                "pick_us": t_pick * 1e6, "pick": list(pick), "best_us": table[bk] * 1e6, "best": list(bk),
@@ -380,15 +402,17 @@ def run_study(args):
         fixed[c] = (s1, _most_frequent(per) if per else None)
 
     def timed_plan(i, plan):
+        # a static plan is timed like the pick and the best (median of 3)
         key = _plan_key(plan)
-        if key not in tables[i]:
+        if key not in dones[i]:
             call, R, keep = _study_ctx(jobs[i], dev, args.rot_mib, L, sp)
             vx.vx_force_plan(*key)
             try:
                 call(0)
-                tables[i][key] = _time_calls(call, R, stream, spin, reps=1)
+                tables[i][key] = _time_calls(call, R, stream, spin)
             finally:
                 vx.vx_force_plan(-1, 0)
+            dones[i].add(key)
             del keep, call
         return key, tables[i][key]
 
