@@ -304,6 +304,12 @@ typedef struct vx_conv2d_desc {
 
 vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void* y, void* stream);
 
+/* Output extent of the convolution `d` (host only): *oh and *ow as defined
+ * above (0 when the numerator is negative).  The same descriptor checks as
+ * vx_conv2d (VX_ERR_INVALID_ARG, VX_ERR_UNSUPPORTED_DTYPE); NULL outputs ->
+ * VX_ERR_INVALID_ARG. */
+vx_status vx_conv2d_output_dims(const vx_conv2d_desc* d, int64_t* oh, int64_t* ow);
+
 /* The plan vx_conv2d would run for `d` (host only, no launch). */
 vx_status vx_conv2d_plan_query(const vx_conv2d_desc* d, vx_plan* out);
 

@@ -589,6 +589,21 @@ vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void*
     return plan_and_launch(sh, a, stream);
 }
 
+vx_status vx_conv2d_output_dims(const vx_conv2d_desc* d, int64_t* oh, int64_t* ow)
+{
+    VxShape sh;
+    VxGemmArgs a = {};
+    bool empty = false;
+    if (!oh || !ow)
+        return VX_ERR_INVALID_ARG;
+    vx_status st = conv_shape(d, &sh, &a, &empty);
+    if (st != VX_OK)
+        return st;
+    *oh = a.cOH;
+    *ow = a.cOW;
+    return VX_OK;
+}
+
 vx_status vx_conv2d_plan_query(const vx_conv2d_desc* d, vx_plan* out)
 {
     VxShape sh;

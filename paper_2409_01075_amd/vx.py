@@ -105,6 +105,8 @@ def lib():
     L.vx_conv2d.restype = i32
     L.vx_conv2d_plan_query.argtypes = [ctypes.POINTER(vx_conv2d_desc), ctypes.POINTER(vx_plan)]
     L.vx_conv2d_plan_query.restype = i32
+    L.vx_conv2d_output_dims.argtypes = [ctypes.POINTER(vx_conv2d_desc), ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    L.vx_conv2d_output_dims.restype = i32
     L.vx_set_workspace.argtypes = [vp, ctypes.c_size_t, vp]
     L.vx_set_workspace.restype = i32
     L.vx_calibration_load.argtypes = [ctypes.c_char_p, ctypes.POINTER(i32)]
@@ -271,9 +273,19 @@ def mi355x_hwinfo():
 
 
 # ------------------------------------------------------ torch helpers -------
+# The C ABI cannot see tensor extents, so the helpers below check everything
+# the kernels will rely on before any library call: ranks, matching inner
+# dimensions, one supported dtype, contiguity, the exact shape and dtype of a
+# caller's `out`, and that every tensor lives on the current GPU (a host
+# pointer or a short `out` handed to a kernel would be an out-of-bounds
+# device access).  Violations raise ValueError.
+
 def _torch_dtype_code(t):
     import torch
-    return {torch.float32: VX_F32, torch.float16: VX_F16, torch.bfloat16: VX_BF16}[t.dtype]
+    codes = {torch.float32: VX_F32, torch.float16: VX_F16, torch.bfloat16: VX_BF16}
+    if t.dtype not in codes:
+        raise ValueError("unsupported dtype %s (float32, float16 or bfloat16)" % t.dtype)
+    return codes[t.dtype]
 
 
 def _stream_ptr(stream):
@@ -282,53 +294,99 @@ def _stream_ptr(stream):
     return s.cuda_stream
 
 
-def gemm(A, B, out=None, stream=None):
-    """C = A @ B for 2-D row-major device tensors (contiguous)."""
+def _check_operands(what, tensors, out, out_shape):
+    """Validates operands (name -> tensor) and the optional `out` against the
+    shape the call will write; returns the dtype code."""
     import torch
+    first = next(iter(tensors.values()))
+    code = _torch_dtype_code(first)
+    for name, t in tensors.items():
+        if t.dtype != first.dtype:
+            raise ValueError("%s: %s has dtype %s, expected %s" % (what, name, t.dtype, first.dtype))
+        if not t.is_contiguous():
+            raise ValueError("%s: %s must be contiguous" % (what, name))
+    if out is not None:
+        if tuple(out.shape) != tuple(out_shape):
+            raise ValueError("%s: out has shape %s, expected %s" % (what, tuple(out.shape), tuple(out_shape)))
+        if out.dtype != first.dtype:
+            raise ValueError("%s: out has dtype %s, expected %s" % (what, out.dtype, first.dtype))
+        if not out.is_contiguous():
+            raise ValueError("%s: out must be contiguous" % what)
+    every = list(tensors.items()) + ([("out", out)] if out is not None else [])
+    for name, t in every:
+        if t.device.type != "cuda":
+            raise ValueError("%s: %s is on %s; every tensor must be on the current GPU" % (what, name, t.device))
+    dev = torch.cuda.current_device()
+    for name, t in every:
+        if t.device.index != dev:
+            raise ValueError("%s: %s is on cuda:%s, the current device is cuda:%d" % (what, name, t.device.index, dev))
+    return code
+
+
+def gemm(A, B, out=None, stream=None):
+    """C = A @ B for 2-D row-major tensors (contiguous, one dtype, current GPU)."""
+    import torch
+    if A.dim() != 2 or B.dim() != 2:
+        raise ValueError("gemm expects 2-D A (M x K) and B (K x N), got %d-D and %d-D" % (A.dim(), B.dim()))
     M, K = A.shape
     K2, N = B.shape
-    if K2 != K or A.dtype != B.dtype or not A.is_contiguous() or not B.is_contiguous():
-        raise ValueError("gemm expects contiguous A (M x K), B (K x N) of one dtype")
+    if K2 != K:
+        raise ValueError("gemm: inner dimensions differ (A is %d x %d, B is %d x %d)" % (M, K, K2, N))
+    code = _check_operands("gemm", {"A": A, "B": B}, out, (M, N))
     C = torch.empty((M, N), dtype=A.dtype, device=A.device) if out is None else out
-    _chk(vx_gemm(M, N, K, _torch_dtype_code(A), A.data_ptr(), B.data_ptr(), C.data_ptr(), _stream_ptr(stream)),
-         "vx_gemm")
+    _chk(vx_gemm(M, N, K, code, A.data_ptr(), B.data_ptr(), C.data_ptr(), _stream_ptr(stream)), "vx_gemm")
     return C
 
 
 def bmm(A, B, out=None, stream=None):
-    """C[b] = A[b] @ B[b] for contiguous 3-D device tensors; B may be 2-D (broadcast)."""
+    """C[b] = A[b] @ B[b] for a 3-D A (batch x M x K) and a 3-D B (batch x K x N),
+    or a 2-D B (K x N) broadcast to every batch; contiguous, one dtype, current GPU."""
     import torch
+    if A.dim() != 3 or B.dim() not in (2, 3):
+        raise ValueError("bmm expects a 3-D A and a 2-D or 3-D B, got %d-D and %d-D" % (A.dim(), B.dim()))
     bt, M, K = A.shape
     if B.dim() == 2:
         K2, N = B.shape
         sB = 0
     else:
-        _, K2, N = B.shape
+        bb, K2, N = B.shape
+        if bb != bt:
+            raise ValueError("bmm: batch sizes differ (%d and %d)" % (bt, bb))
         sB = K2 * N
-    if K2 != K or A.dtype != B.dtype or not A.is_contiguous() or not B.is_contiguous():
-        raise ValueError("bmm expects contiguous operands of one dtype")
+    if K2 != K:
+        raise ValueError("bmm: inner dimensions differ (A is .. x %d x %d, B is .. x %d x %d)" % (M, K, K2, N))
+    code = _check_operands("bmm", {"A": A, "B": B}, out, (bt, M, N))
     C = torch.empty((bt, M, N), dtype=A.dtype, device=A.device) if out is None else out
-    _chk(vx_gemm_batched(bt, M, N, K, _torch_dtype_code(A), A.data_ptr(), M * K, B.data_ptr(), sB,
+    _chk(vx_gemm_batched(bt, M, N, K, code, A.data_ptr(), M * K, B.data_ptr(), sB,
                          C.data_ptr(), M * N, _stream_ptr(stream)), "vx_gemm_batched")
     return C
 
 
+def conv2d_output_shape(x_shape, w_shape, stride=(1, 1), padding=(0, 0), dilation=(1, 1)):
+    """(N, OH, OW, Cout) of conv2d(x, w) as the library computes it
+    (vx_conv2d_output_dims)."""
+    N, H, W, Cin = x_shape
+    KH, KW, _, Cout = w_shape
+    d = conv_desc(N, H, W, Cin, Cout, KH, KW, VX_F16, stride, padding, dilation)
+    oh, ow = ctypes.c_int64(), ctypes.c_int64()
+    _chk(lib().vx_conv2d_output_dims(ctypes.byref(d), ctypes.byref(oh), ctypes.byref(ow)), "vx_conv2d_output_dims")
+    return (N, oh.value, ow.value, Cout)
+
+
 def conv2d(x, w, stride=(1, 1), padding=(0, 0), dilation=(1, 1), out=None, stream=None):
     """y = conv2d(x, w) for torch tensors: x N x H x W x Cin, w KH x KW x Cin x Cout
-    (both contiguous, same dtype, on the current device); returns y N x OH x OW x Cout."""
+    (both contiguous, same dtype, on the current GPU); returns y N x OH x OW x Cout."""
     import torch
-    if x.dim() != 4 or w.dim() != 4 or x.shape[3] != w.shape[2] or x.dtype != w.dtype:
-        raise ValueError("conv2d: x must be N x H x W x Cin, w KH x KW x Cin x Cout, same dtype")
-    if not (x.is_contiguous() and w.is_contiguous()):
-        raise ValueError("conv2d: operands must be contiguous")
-    N, H, W, Cin = x.shape
-    KH, KW, _, Cout = w.shape
-    span_h = H + 2 * padding[0] - dilation[0] * (KH - 1) - 1
-    span_w = W + 2 * padding[1] - dilation[1] * (KW - 1) - 1
-    OH = span_h // stride[0] + 1 if span_h >= 0 else 0
-    OW = span_w // stride[1] + 1 if span_w >= 0 else 0
+    if x.dim() != 4 or w.dim() != 4:
+        raise ValueError("conv2d: x must be N x H x W x Cin and w KH x KW x Cin x Cout")
+    if x.shape[3] != w.shape[2]:
+        raise ValueError("conv2d: x has %d channels, w expects %d" % (x.shape[3], w.shape[2]))
+    _check_operands("conv2d", {"x": x, "w": w}, None, None)
+    shape = conv2d_output_shape(tuple(x.shape), tuple(w.shape), stride, padding, dilation)
+    code = _check_operands("conv2d", {"x": x, "w": w}, out, shape)
     if out is None:
-        out = torch.empty((N, OH, OW, Cout), dtype=x.dtype, device=x.device)
-    d = conv_desc(N, H, W, Cin, Cout, KH, KW, _torch_dtype_code(x), stride, padding, dilation)
+        out = torch.empty(shape, dtype=x.dtype, device=x.device)
+    d = conv_desc(*shape[:1], x.shape[1], x.shape[2], x.shape[3], shape[3], w.shape[0], w.shape[1], code,
+                  stride, padding, dilation)
     _chk(vx_conv2d(d, x.data_ptr(), w.data_ptr(), out.data_ptr(), _stream_ptr(stream)), "vx_conv2d")
     return out
