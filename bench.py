@@ -204,34 +204,8 @@ def _set_jobs(name, trials, shapes="", dtype="bf16"):
             A, B = I.single_f32(0)
             return torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
         return [("fp32 77x96x80", 1, 77, 96, 80, 0, mk)]
-    if name == "encoder":
-        for t in range(64 if trials is None else trials):
-            M = I.encoder_shape(t)
-            for gi, (K, N) in enumerate(I.ENCODER_SHAPES):
-                def mk(dev, t=t, gi=gi, M=M, K=K, N=N):
-                    return (I.device_normal((M, K), 1.0, 1000 * t + 2 * gi, dev, bf),
-                            I.device_normal((K, N), 0.02, 1000 * t + 2 * gi + 1, dev, bf))
-                jobs.append(("t%d G%d (%d,%d)x(%d,%d)" % (t, gi + 1, M, K, K, N), 1, M, N, K, 2, mk))
-    elif name == "llm":
-        for t in range(48 if trials is None else trials):
-            M = I.llm_M(t)
-            for gi, (K, N) in enumerate(I.LLM_SHAPES):
-                def mk(dev, t=t, gi=gi, M=M, K=K, N=N):
-                    return (I.device_normal((M, K), 1.0, 1000 * t + 2 * gi, dev, bf),
-                            I.device_normal((K, N), 0.02, 1000 * t + 2 * gi + 1, dev, bf))
-                jobs.append(("t%d H%d (%d,%d)x(%d,%d)" % (t, gi + 1, M, K, K, N), 1, M, N, K, 2, mk))
-    elif name == "attention":
-        b, d = I.ATTN_BATCH, I.ATTN_HEAD
-        for t in range(32 if trials is None else trials):
-            L = I.attention_L(t)
-            def mk_s(dev, t=t, L=L):
-                return (I.device_normal((b, L, d), 1.0, 1000 * t, dev, bf),
-                        I.device_normal((b, d, L), 1.0, 1000 * t + 1, dev, bf))
-            def mk_o(dev, t=t, L=L):
-                return (I.device_softmax_rows((b, L, L), 1000 * t + 2, dev, bf),
-                        I.device_normal((b, L, d), 1.0, 1000 * t + 3, dev, bf))
-            jobs.append(("t%d S L=%d" % (t, L), b, L, L, d, 2, mk_s))
-            jobs.append(("t%d O L=%d" % (t, L), b, L, d, L, 2, mk_o))
+    if name in ("encoder", "llm", "attention"):
+        jobs = [(label, b, M, N, K, 2, mk) for (label, b, M, N, K, mk) in I.device_set(name, trials)]
     return jobs
 
 

@@ -267,6 +267,15 @@ vx_status vx_enable_hybrid_grid(int enable);
 vx_status vx_enable_k_rotation(int enable);
 
 /*
+ * Test hook for the split-K workspace fallback: with fail != 0 the library's
+ * own lazily allocated workspace is treated as unavailable, so calls on a
+ * stream without a workspace plan without split-K (as they do when the
+ * allocation really fails), and plan queries report such plans.  0 restores
+ * normal behaviour.  Process-wide; for tests.
+ */
+vx_status vx_test_fail_workspace_alloc(int fail);
+
+/*
  * Hand the library a caller-owned device buffer to use as the split-K
  * workspace of `stream` (NULL/0 bytes: return to the library's own lazily
  * allocated buffer).  The buffer must stay valid until the stream's work

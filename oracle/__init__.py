@@ -40,6 +40,9 @@ def _load():
     lib.oracle_gemm_sampled.argtypes = [ip, i64, i64, i64, vp, i64, vp, i64, i64,
                                         vp, vp, vp, dp, dp]
     lib.oracle_gemm_sampled.restype = ctypes.c_int
+    lib.oracle_gemm_sampled_mt.argtypes = [ip, i64, i64, i64, vp, i64, vp, i64, i64,
+                                           vp, vp, vp, dp, dp, ip]
+    lib.oracle_gemm_sampled_mt.restype = ctypes.c_int
     lib.oracle_conv2d.argtypes = [ip] + [i64] * 13 + [vp, vp, dp, dp, ip]
     lib.oracle_conv2d.restype = ctypes.c_int
     lib.oracle_conv_out_dim.argtypes = [i64] * 5
@@ -137,8 +140,12 @@ def gemm(A, B, dtype, M=None, N=None, K=None, batch=1, sA=None, sB=None,
     return (C, G) if with_mag else C
 
 
-def gemm_sampled(A, B, dtype, M, N, K, rows, cols, bats=None, sA=None, sB=None):
-    """Reference values at the sampled positions only: (ref, mag) float64 vectors."""
+def gemm_sampled(A, B, dtype, M, N, K, rows, cols, bats=None, sA=None, sB=None, threads=1):
+    """Reference values at the sampled positions only: (ref, mag) float64 vectors.
+
+    threads > 1 shares the samples over that many threads (visited grouped by
+    batch and column, so a strided column of B is decoded once per group);
+    every value is the same binary64 sum either way."""
     code = dtype_code(dtype)
     a = _as_storage(A, code)
     b = _as_storage(B, code)
@@ -156,9 +163,22 @@ def gemm_sampled(A, B, dtype, M, N, K, rows, cols, bats=None, sA=None, sB=None):
             raise ValueError("operand storage too small for the sampled batches")
     ref = np.empty(n, dtype=np.float64)
     mag = np.empty(n, dtype=np.float64)
-    rc = _load().oracle_gemm_sampled(code, M, N, K, a.ctypes.data, sA, b.ctypes.data, sB, n,
-                                     bats.ctypes.data, rows.ctypes.data, cols.ctypes.data,
-                                     ref.ctypes.data, mag.ctypes.data)
+    if threads is None or threads > 1:
+        order = np.lexsort((rows, cols, bats))
+        r_ = np.ascontiguousarray(rows[order])
+        c_ = np.ascontiguousarray(cols[order])
+        b_ = np.ascontiguousarray(bats[order])
+        ref_s = np.empty(n, dtype=np.float64)
+        mag_s = np.empty(n, dtype=np.float64)
+        rc = _load().oracle_gemm_sampled_mt(code, M, N, K, a.ctypes.data, sA, b.ctypes.data, sB, n,
+                                            b_.ctypes.data, r_.ctypes.data, c_.ctypes.data,
+                                            ref_s.ctypes.data, mag_s.ctypes.data, threads or default_threads())
+        ref[order] = ref_s
+        mag[order] = mag_s
+    else:
+        rc = _load().oracle_gemm_sampled(code, M, N, K, a.ctypes.data, sA, b.ctypes.data, sB, n,
+                                         bats.ctypes.data, rows.ctypes.data, cols.ctypes.data,
+                                         ref.ctypes.data, mag.ctypes.data)
     if rc != 0:
         raise RuntimeError("oracle_gemm_sampled failed (rc=%d)" % rc)
     return ref, mag

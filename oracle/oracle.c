@@ -271,6 +271,104 @@ int oracle_gemm_sampled(int dtype, int64_t M, int64_t N, int64_t K,
     return 0;
 }
 
+/*
+ * The same sampled values with the samples shared over `threads` threads.
+ * Each sample's sum is exactly the one above (k ascending, the same decoded
+ * products); a thread only keeps the decoded column of B of its previous
+ * sample when the next one reads the same (batch, column), so callers that
+ * list samples grouped by column read each strided column once.
+ */
+typedef struct {
+    int dtype;
+    int64_t M, N, K, sA, sB, s0, s1;
+    const char *A, *B;
+    const int64_t *bat, *row, *col;
+    double *ref, *mag;
+    int bad;
+} samp_job;
+
+static void *samp_rows(void *arg)
+{
+    samp_job *j = (samp_job *)arg;
+    size_t es = elem_size(j->dtype);
+    double *bcol = (double *)malloc(sizeof(double) * (size_t)(j->K > 0 ? j->K : 1));
+    int64_t cur_b = -1, cur_c = -1, s, k;
+    if (!bcol) {
+        j->bad = 1;
+        return NULL;
+    }
+    for (s = j->s0; s < j->s1; ++s) {
+        if (j->row[s] < 0 || j->row[s] >= j->M || j->col[s] < 0 || j->col[s] >= j->N || j->bat[s] < 0) {
+            j->bad = 1;
+            break;
+        }
+        if (j->bat[s] != cur_b || j->col[s] != cur_c) {
+            const char *Bb = j->B + (size_t)(j->bat[s] * j->sB) * es;
+            for (k = 0; k < j->K; ++k)
+                oracle_decode(j->dtype, Bb + (size_t)(k * j->N + j->col[s]) * es, &bcol[k], 1);
+            cur_b = j->bat[s];
+            cur_c = j->col[s];
+        }
+        const char *Ar = j->A + (size_t)(j->bat[s] * j->sA + j->row[s] * j->K) * es;
+        double acc = 0.0, m = 0.0;
+        for (k = 0; k < j->K; ++k) {
+            double a;
+            oracle_decode(j->dtype, Ar + (size_t)k * es, &a, 1);
+            acc += a * bcol[k];
+            m += fabs(a) * fabs(bcol[k]);
+        }
+        j->ref[s] = acc;
+        if (j->mag)
+            j->mag[s] = m;
+    }
+    free(bcol);
+    return NULL;
+}
+
+int oracle_gemm_sampled_mt(int dtype, int64_t M, int64_t N, int64_t K,
+                           const void *A, int64_t sA, const void *B, int64_t sB,
+                           int64_t nsamp, const int64_t *bat, const int64_t *row,
+                           const int64_t *col, double *ref, double *mag, int threads)
+{
+    if (M < 0 || N < 0 || K < 0 || nsamp < 0 || dtype < 0 || dtype > 2)
+        return -1;
+    if (threads < 1)
+        threads = 1;
+    if (threads > nsamp)
+        threads = nsamp > 0 ? (int)nsamp : 1;
+    pthread_t *tid = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)threads);
+    samp_job *jobs = (samp_job *)malloc(sizeof(samp_job) * (size_t)threads);
+    if (!tid || !jobs) {
+        free(tid);
+        free(jobs);
+        return -2;
+    }
+    int t, bad = 0;
+    for (t = 0; t < threads; ++t) {
+        samp_job j = {dtype, M, N, K, sA, sB, nsamp * t / threads, nsamp * (t + 1) / threads,
+                      (const char *)A, (const char *)B, bat, row, col, ref, mag, 0};
+        jobs[t] = j;
+    }
+    /* a thread that cannot be started leaves its samples to the caller's thread */
+    char *run = (char *)calloc((size_t)threads, 1);
+    for (t = 1; t < threads; ++t)
+        run[t] = run != NULL && pthread_create(&tid[t], NULL, samp_rows, &jobs[t]) == 0;
+    samp_rows(&jobs[0]);
+    for (t = 1; t < threads; ++t) {
+        if (run && run[t])
+            pthread_join(tid[t], NULL);
+        else
+            samp_rows(&jobs[t]);
+    }
+    for (t = 0; t < threads; ++t)
+        if (jobs[t].bad)
+            bad = -1;
+    free(run);
+    free(tid);
+    free(jobs);
+    return bad;
+}
+
 /* ---- the 2-D convolution ------------------------------------------------ */
 
 /*

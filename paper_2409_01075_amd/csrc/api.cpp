@@ -28,7 +28,7 @@ std::mutex& g_calib_try_mu()
     static std::mutex m;
     return m;
 }
-bool g_override_set = false;
+std::atomic<bool> g_override_set{false};
 vx_hwinfo g_override;
 bool g_hw_valid[kMaxDevices];
 vx_hwinfo g_hw[kMaxDevices];
@@ -39,31 +39,95 @@ std::atomic<int> g_backends{3};   // kernel backends the selector may use (vx_re
 std::atomic<bool> g_hybrid{true};  // hybrid grids among the plans (vx_enable_hybrid_grid)
 std::atomic<bool> g_krot{true};    // rotated K order in the direct-to-LDS GEMM kernels (vx_enable_k_rotation)
 std::atomic<uint64_t> g_epoch{0};   // bumps when planning inputs change
+std::atomic<bool> g_fail_ws_alloc{false};   // test hook: the lazy workspace allocation fails
 
 struct PlanKey {
     int64_t batch, M, N, K;
     int dt, vec_ok, c_vec, dev;
     size_t ws;
+    int64_t tickets;
     uint64_t epoch;
     int op;
     bool operator==(const PlanKey& o) const
     {
         return batch == o.batch && M == o.M && N == o.N && K == o.K && dt == o.dt && vec_ok == o.vec_ok &&
-               c_vec == o.c_vec && dev == o.dev && ws == o.ws && epoch == o.epoch && op == o.op;
+               c_vec == o.c_vec && dev == o.dev && ws == o.ws && tickets == o.tickets && epoch == o.epoch &&
+               op == o.op;
     }
 };
-struct PlanKeyHash {
-    size_t operator()(const PlanKey& k) const
+uint64_t plan_hash(const PlanKey& k)
+{
+    uint64_t h = 1469598103934665603ull;
+    auto mix = [&h](uint64_t v) { h = (h ^ v) * 1099511628211ull; };
+    mix(k.batch); mix(k.M); mix(k.N); mix(k.K);
+    mix(k.dt | (k.vec_ok << 4) | (k.c_vec << 5) | (k.op << 6) | ((uint64_t)k.dev << 8));
+    mix(k.ws); mix(k.tickets); mix(k.epoch);
+    return h ^ (h >> 29);
+}
+
+// Plan cache: a fixed table in static storage (nothing is allocated when a
+// shape is first seen), 4-way probed, under g_mu; plus each thread's last
+// plan, which repeated calls of one shape find without taking the lock.
+// Entries carry the planning epoch, so a change of the planning inputs
+// (calibration, overrides, ablation switches, workspaces) retires them all.
+constexpr int kPlanSlots = 4096;   // a power of two
+constexpr int kPlanProbe = 4;
+struct PlanSlot {
+    PlanKey key;
+    vx_plan plan;
+    bool used;
+};
+PlanSlot g_slots[kPlanSlots];
+unsigned g_slot_victim = 0;
+struct LastPlan {
+    PlanKey key;
+    vx_plan plan;
+    bool valid;
+};
+thread_local LastPlan t_last = {};
+
+bool cache_find(const PlanKey& k, vx_plan* out)
+{
+    if (t_last.valid && t_last.key == k) {
+        *out = t_last.plan;
+        return true;
+    }
+    const uint64_t h = plan_hash(k);
+    std::lock_guard<std::mutex> lk(g_mu);
+    for (int i = 0; i < kPlanProbe; ++i) {
+        const PlanSlot& e = g_slots[(h + i) & (kPlanSlots - 1)];
+        if (e.used && e.key == k) {
+            *out = e.plan;
+            t_last.key = k;
+            t_last.plan = e.plan;
+            t_last.valid = true;
+            return true;
+        }
+    }
+    return false;
+}
+
+void cache_put(const PlanKey& k, const vx_plan& p)
+{
+    const uint64_t h = plan_hash(k);
     {
-        uint64_t h = 1469598103934665603ull;
-        auto mix = [&h](uint64_t v) { h = (h ^ v) * 1099511628211ull; };
-        mix(k.batch); mix(k.M); mix(k.N); mix(k.K);
-        mix(k.dt | (k.vec_ok << 4) | (k.c_vec << 5) | (k.op << 6) | ((uint64_t)k.dev << 8));
-        mix(k.ws); mix(k.epoch);
-        return (size_t)h;
+        std::lock_guard<std::mutex> lk(g_mu);
+        int slot = -1;
+        for (int i = 0; i < kPlanProbe && slot < 0; ++i) {
+            const PlanSlot& e = g_slots[(h + i) & (kPlanSlots - 1)];
+            if (!e.used || e.key.epoch != k.epoch || e.key == k)
+                slot = (int)((h + i) & (kPlanSlots - 1));
+        }
+        if (slot < 0)
+            slot = (int)((h + (g_slot_victim++ % kPlanProbe)) & (kPlanSlots - 1));
+        g_slots[slot].key = k;
+        g_slots[slot].plan = p;
+        g_slots[slot].used = true;
     }
-};
-std::unordered_map<PlanKey, vx_plan, PlanKeyHash> g_plans;
+    t_last.key = k;
+    t_last.plan = p;
+    t_last.valid = true;
+}
 
 struct Workspace {
     char* base = nullptr;
@@ -137,7 +201,6 @@ int load_calib_file(const char* path, const char* arch)
         g_calib.swap(cal);
         g_calib_ok.swap(ok);
         g_calib_launch_ns = launch;
-        g_plans.clear();
     }
     g_calib_loaded.store(true);
     g_epoch.fetch_add(1);
@@ -205,14 +268,18 @@ vx_status current_device(int* dev)
     return VX_OK;
 }
 
-vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
+vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, int64_t tickets, vx_plan* out)
 {
     // the epoch is read before the filter: a setter changes the filter and
     // then bumps the epoch, so a plan made under a stale filter is filed
     // under a stale epoch and never found again
     const uint64_t epoch = g_epoch.load();
+    const int forced = g_force_id.load();
+    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, tickets, epoch, sh.op};
+    if (forced < 0 && cache_find(key, out))
+        return VX_OK;
     VxFilter f;
-    f.kernel_id = g_force_id.load();
+    f.kernel_id = forced;
     f.split = g_force_split.load();
     f.wave_m = g_fix_wm.load();
     f.wave_n = g_fix_wn.load();
@@ -226,40 +293,60 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, vx_plan* out)
     ensure_calib(hw);
     VxLimits lim;
     lim.ws_bytes = ws_bytes;
-    lim.max_tickets = ws_bytes ? (int64_t)(kTicketBytes / 4) : 0;
-    if (f.kernel_id >= 0)
-        return vxi_select(hw, sh, lim, f, out);
-    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, epoch, sh.op};
-    {
-        std::lock_guard<std::mutex> lk(g_mu);
-        auto it = g_plans.find(key);
-        if (it != g_plans.end()) {
-            *out = it->second;
-            return VX_OK;
-        }
-    }
+    lim.max_tickets = ws_bytes ? tickets : 0;
     st = vxi_select(hw, sh, lim, f, out);
-    if (st != VX_OK)
-        return st;
-    std::lock_guard<std::mutex> lk(g_mu);
-    if (g_plans.size() > (1u << 20))
-        g_plans.clear();
-    g_plans.emplace(key, *out);
-    return VX_OK;
+    if (st == VX_OK && forced < 0)
+        cache_put(key, *out);
+    return st;
 }
 
-// Workspace of (device, stream): returns its capacity for partials (0 if none yet).
+// ---- split-K workspace -------------------------------------------------------
+// Default calls: one buffer per (device, stream), the caller's (vx_set_workspace)
+// or allocated by the library at the first call that plans split-K.
+// vx_gemm_batched_noalloc: the static scratch array of its device.  Either way
+// the arrival counters come first, then the fp32 partials.
+struct WsView {
+    char* base;             // counters at base, partials at base + ticket_bytes
+    size_t ticket_bytes;
+    size_t partial_bytes;
+};
+std::atomic<uint64_t> g_ws_epoch{1};   // bumps when a (device, stream) workspace changes
+struct LastWs {
+    int dev;
+    void* stream;
+    uint64_t epoch;
+    size_t capacity;
+    Workspace ws;
+    bool valid;
+};
+thread_local LastWs t_ws = {};
+
+// Capacity for partials of (device, stream)'s workspace: the default size if
+// the library will allocate it at first use (0 while the test hook says that
+// allocation fails).
 size_t ws_capacity(int dev, void* stream)
 {
+    const uint64_t ep = g_ws_epoch.load();
+    if (g_fail_ws_alloc.load())
+        return 0;
+    if (t_ws.valid && t_ws.dev == dev && t_ws.stream == stream && t_ws.epoch == ep)
+        return t_ws.capacity;
     std::lock_guard<std::mutex> lk(g_mu);
     auto it = g_ws.find({dev, stream});
     if (it == g_ws.end())
         return kDefaultPartials;   // will be allocated on first use
-    return it->second.bytes > kTicketBytes ? it->second.bytes - kTicketBytes : 0;
+    t_ws = LastWs{dev, stream, ep, it->second.bytes > kTicketBytes ? it->second.bytes - kTicketBytes : 0,
+                  it->second, true};
+    return t_ws.capacity;
 }
 
 vx_status ws_get(int dev, void* stream, Workspace* out)
 {
+    const uint64_t ep = g_ws_epoch.load();
+    if (t_ws.valid && t_ws.dev == dev && t_ws.stream == stream && t_ws.epoch == ep) {
+        *out = t_ws.ws;
+        return VX_OK;
+    }
     std::lock_guard<std::mutex> lk(g_mu);
     auto key = std::make_pair(dev, stream);
     auto it = g_ws.find(key);
@@ -267,6 +354,8 @@ vx_status ws_get(int dev, void* stream, Workspace* out)
         *out = it->second;
         return VX_OK;
     }
+    if (g_fail_ws_alloc.load())
+        return VX_ERR_WORKSPACE;
     Workspace w;
     if (hipMalloc((void**)&w.base, kTicketBytes + kDefaultPartials) != hipSuccess) {
         (void)hipGetLastError();
@@ -279,14 +368,111 @@ vx_status ws_get(int dev, void* stream, Workspace* out)
         return VX_ERR_WORKSPACE;
     }
     g_ws[key] = w;
+    g_ws_epoch.fetch_add(1);
     *out = w;
     return VX_OK;
 }
 
-vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream);
+// Per-device launch facts of the hardware description (constant unless the
+// planning override changes, which bumps the epoch).
+struct LastHw {
+    int dev;
+    uint64_t epoch;
+    int num_xcd;
+    double l2_bytes_per_xcd;
+    bool valid;
+};
+thread_local LastHw t_hw = {};
 
-vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
-                    int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, void* stream)
+// Plans shape `sh` on the current device and launches the chosen kernel with
+// the operand fields of `a` (pointers, batch strides, convolution shape);
+// the size and grid fields are filled in here.  scratch == nullptr: the
+// (device, stream) workspace; otherwise the given buffer, and nothing is
+// allocated.
+vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream, const WsView* scratch)
+{
+    int dev = 0;
+    vx_status st = current_device(&dev);
+    if (st != VX_OK)
+        return st;
+    if (dev < 0)
+        return VX_ERR_HIP;   // planning override without a device: nothing to launch on
+
+    vx_plan plan;
+    WsView ws = {nullptr, kTicketBytes, 0};
+    if (scratch) {
+        ws = *scratch;
+        st = plan_for(dev, sh, ws.partial_bytes, (int64_t)(ws.ticket_bytes / 4), &plan);
+        if (st == VX_ERR_NO_CANDIDATE && g_force_id.load() >= 0) {
+            // a forced plan that only fails for want of scratch space
+            vx_plan unused;
+            if (plan_for(dev, sh, kDefaultPartials, (int64_t)(kTicketBytes / 4), &unused) == VX_OK)
+                return VX_ERR_WORKSPACE;
+        }
+        if (st != VX_OK)
+            return st;
+        if (plan.split_k > 1 && plan.workspace_bytes > ws.partial_bytes)
+            return VX_ERR_WORKSPACE;
+    } else {
+        st = plan_for(dev, sh, ws_capacity(dev, stream), (int64_t)(kTicketBytes / 4), &plan);
+        if (st != VX_OK)
+            return st;
+        if (plan.split_k > 1) {
+            Workspace w;
+            if (ws_get(dev, stream, &w) != VX_OK) {
+                st = plan_for(dev, sh, 0, 0, &plan);   // fall back to plans without split-K
+                if (st != VX_OK)
+                    return st;
+            } else {
+                ws.base = w.base;
+            }
+        }
+    }
+    int n = 0;
+    const VxKernelEntry* reg = vxi_registry(&n);
+    if (plan.kernel_id < 0 || plan.kernel_id >= n)
+        return VX_ERR_NO_CANDIDATE;
+
+    const uint64_t ep = g_epoch.load();
+    if (!(t_hw.valid && t_hw.dev == dev && t_hw.epoch == ep)) {
+        vx_hwinfo hw;
+        st = hwinfo_for(dev, &hw);
+        if (st != VX_OK)
+            return st;
+        t_hw = LastHw{dev, ep, hw.num_xcd, hw.l2_bytes_per_xcd, true};
+    }
+
+    a.M = (int)sh.M;
+    a.N = (int)sh.N;
+    a.K = (int)sh.K;
+    a.tiles_m = (int)plan.tiles_m;
+    a.tiles_n = (int)plan.tiles_n;
+    a.split = plan.split_k;
+    a.k_per_split = plan.k_per_split;
+    a.batch = (int)sh.batch;
+    a.group_m = plan.group_m;
+    a.num_xcd = t_hw.num_xcd;
+    a.grid = (int)plan.grid;
+    a.dp_tiles = (int)plan.dp_tiles;
+    // rotated K order where one batch entry's operands stay resident in an
+    // XCD's L2 (the plain-ring direct-to-LDS kernels read it)
+    a.krot = g_krot.load() && (double)(sh.M * sh.K + sh.K * sh.N) * elem_bytes(sh.dt) <= t_hw.l2_bytes_per_xcd ? 1 : 0;
+    a.ws = plan.split_k > 1 ? (float*)(ws.base + ws.ticket_bytes) : nullptr;
+    a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
+    hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return VX_ERR_HIP;
+    }
+    return VX_OK;
+}
+
+// Argument checks of a (batched) GEMM call, before any HIP call; fills the
+// selector's view of the shape and the operand fields of the launch
+// arguments.  *noop: nothing to compute (M, N or batch is 0).
+vx_status gemm_prepare(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                       int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, VxShape* sh, VxGemmArgs* a,
+                       bool* noop)
 {
     if (dtype != VX_F32 && dtype != VX_F16 && dtype != VX_BF16)
         return VX_ERR_UNSUPPORTED_DTYPE;
@@ -302,90 +488,66 @@ vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dty
         return VX_ERR_INVALID_ARG;
     if (overlaps(C, ec * eb, A, ea * eb) || overlaps(C, ec * eb, B, eb_ * eb))
         return VX_ERR_INVALID_ARG;
-    if (batch == 0 || M == 0 || N == 0)
+    *noop = batch == 0 || M == 0 || N == 0;
+    if (*noop)
         return VX_OK;
-
-    VxShape sh;
-    sh.batch = batch;
-    sh.M = M;
-    sh.N = N;
-    sh.K = K;
-    sh.dt = dtype;
+    sh->batch = batch;
+    sh->M = M;
+    sh->N = N;
+    sh->K = K;
+    sh->dt = dtype;
     const int ve = 16 / eb;
     // per operand: every row starts on a 16-byte boundary
     const bool a_vec = (K % ve == 0) && ((uintptr_t)A % 16 == 0) && (batch == 1 || sA % ve == 0);
     const bool b_vec = (N % ve == 0) && ((uintptr_t)B % 16 == 0) && (batch == 1 || sB % ve == 0);
-    sh.vec_ok = (a_vec ? 1 : 0) | (b_vec ? 2 : 0);
-    sh.c_vec = (N % 4 == 0) && ((uintptr_t)C % (4 * eb) == 0) && (batch == 1 || sC % 4 == 0);
-
-    VxGemmArgs a = {};
-    a.A = A;
-    a.B = B;
-    a.C = C;
-    a.sA = sA;
-    a.sB = sB;
-    a.sC = sC;
-    return plan_and_launch(sh, a, stream);
+    sh->vec_ok = (a_vec ? 1 : 0) | (b_vec ? 2 : 0);
+    sh->c_vec = (N % 4 == 0) && ((uintptr_t)C % (4 * eb) == 0) && (batch == 1 || sC % 4 == 0);
+    *a = VxGemmArgs{};
+    a->A = A;
+    a->B = B;
+    a->C = C;
+    a->sA = sA;
+    a->sB = sB;
+    a->sC = sC;
+    return VX_OK;
 }
 
-// Plans shape `sh` on the current device and launches the chosen kernel with
-// the operand fields of `a` (pointers, batch strides, convolution shape);
-// the size and grid fields are filled in here.
-vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream)
+}  // namespace
+
+vx_status vxi_gemm_check(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                         int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, bool* noop)
 {
-    int dev = 0;
-    vx_status st = current_device(&dev);
-    if (st != VX_OK)
+    VxShape sh;
+    VxGemmArgs a;
+    return gemm_prepare(batch, M, N, K, dtype, A, sA, B, sB, C, sC, &sh, &a, noop);
+}
+
+vx_status vxi_gemm_scratch(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                           int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, void* stream,
+                           void* scratch, size_t ticket_bytes, size_t partial_bytes)
+{
+    VxShape sh;
+    VxGemmArgs a;
+    bool noop = false;
+    const vx_status st = gemm_prepare(batch, M, N, K, dtype, A, sA, B, sB, C, sC, &sh, &a, &noop);
+    if (st != VX_OK || noop)
         return st;
-    if (dev < 0)
-        return VX_ERR_HIP;   // planning override without a device: nothing to launch on
+    const WsView view = {(char*)scratch, ticket_bytes, partial_bytes};
+    return plan_and_launch(sh, a, stream, &view);
+}
 
-    vx_plan plan;
-    st = plan_for(dev, sh, ws_capacity(dev, stream), &plan);
-    if (st != VX_OK)
+namespace {
+
+vx_status gemm_impl(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                    int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, void* stream)
+{
+    VxShape sh;
+    VxGemmArgs a;
+    bool noop = false;
+    const vx_status st = gemm_prepare(batch, M, N, K, dtype, A, sA, B, sB, C, sC, &sh, &a, &noop);
+    if (st != VX_OK || noop)
         return st;
-
-    Workspace ws;
-    if (plan.split_k > 1) {
-        if (ws_get(dev, stream, &ws) != VX_OK) {
-            st = plan_for(dev, sh, 0, &plan);   // fall back to plans without split-K
-            if (st != VX_OK)
-                return st;
-        }
-    }
-    int n = 0;
-    const VxKernelEntry* reg = vxi_registry(&n);
-    if (plan.kernel_id < 0 || plan.kernel_id >= n)
-        return VX_ERR_NO_CANDIDATE;
-
-    vx_hwinfo hw;
-    st = hwinfo_for(dev, &hw);
-    if (st != VX_OK)
-        return st;
-
-    a.M = (int)sh.M;
-    a.N = (int)sh.N;
-    a.K = (int)sh.K;
-    a.tiles_m = (int)plan.tiles_m;
-    a.tiles_n = (int)plan.tiles_n;
-    a.split = plan.split_k;
-    a.k_per_split = plan.k_per_split;
-    a.batch = (int)sh.batch;
-    a.group_m = plan.group_m;
-    a.num_xcd = hw.num_xcd;
-    a.grid = (int)plan.grid;
-    a.dp_tiles = (int)plan.dp_tiles;
-    // rotated K order where one batch entry's operands stay resident in an
-    // XCD's L2 (the plain-ring direct-to-LDS kernels read it)
-    a.krot = g_krot.load() && (double)(sh.M * sh.K + sh.K * sh.N) * elem_bytes(sh.dt) <= hw.l2_bytes_per_xcd ? 1 : 0;
-    a.ws = plan.split_k > 1 ? (float*)(ws.base + kTicketBytes) : nullptr;
-    a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
-    hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return VX_ERR_HIP;
-    }
-    return VX_OK;
+    return plan_and_launch(sh, a, stream, nullptr);
 }
 
 int64_t conv_out_dim(int64_t in, int64_t k, int64_t stride, int64_t pad, int64_t dil)
@@ -480,7 +642,6 @@ vx_status vx_calibration_load(const char* path, int* n_loaded)
         // no usable default table: the selector is purely analytical
         g_calib_loaded.store(false);
         std::lock_guard<std::mutex> lk(g_mu);
-        g_plans.clear();
         g_epoch.fetch_add(1);
     }
     if (n_loaded)
@@ -492,7 +653,6 @@ vx_status vx_calibration_enable(int enable)
 {
     g_calib_enabled.store(enable != 0);
     std::lock_guard<std::mutex> lk(g_mu);
-    g_plans.clear();
     g_epoch.fetch_add(1);
     return VX_OK;
 }
@@ -562,7 +722,8 @@ vx_status vx_plan_query(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype
     vx_status st = current_device(&dev);
     if (st != VX_OK)
         return st;
-    return plan_for(dev, sh, dev < 0 ? kDefaultPartials : ws_capacity(dev, nullptr), out);
+    const size_t cap = g_fail_ws_alloc.load() ? 0 : dev < 0 ? kDefaultPartials : ws_capacity(dev, nullptr);
+    return plan_for(dev, sh, cap, (int64_t)(kTicketBytes / 4), out);
 }
 
 vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void* y, void* stream)
@@ -586,7 +747,7 @@ vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void*
     a.A = x;
     a.B = w;
     a.C = y;
-    return plan_and_launch(sh, a, stream);
+    return plan_and_launch(sh, a, stream, nullptr);
 }
 
 vx_status vx_conv2d_output_dims(const vx_conv2d_desc* d, int64_t* oh, int64_t* ow)
@@ -618,7 +779,8 @@ vx_status vx_conv2d_plan_query(const vx_conv2d_desc* d, vx_plan* out)
     st = current_device(&dev);
     if (st != VX_OK)
         return st;
-    return plan_for(dev, sh, dev < 0 ? kDefaultPartials : ws_capacity(dev, nullptr), out);
+    const size_t cap = g_fail_ws_alloc.load() ? 0 : dev < 0 ? kDefaultPartials : ws_capacity(dev, nullptr);
+    return plan_for(dev, sh, cap, (int64_t)(kTicketBytes / 4), out);
 }
 
 vx_status vx_plan_cost(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, int kernel_id,
@@ -674,7 +836,6 @@ vx_status vx_set_hwinfo_override(const vx_hwinfo* hw)
     g_override_set = hw != nullptr;
     if (hw)
         g_override = *hw;
-    g_plans.clear();
     g_epoch.fetch_add(1);
     return VX_OK;
 }
@@ -720,7 +881,6 @@ vx_status vx_restrict_backends(int mask)
         return VX_ERR_NO_CANDIDATE;
     std::lock_guard<std::mutex> lk(g_mu);
     g_backends.store(mask);
-    g_plans.clear();
     g_epoch.fetch_add(1);
     return VX_OK;
 }
@@ -729,7 +889,6 @@ vx_status vx_enable_hybrid_grid(int enable)
 {
     std::lock_guard<std::mutex> lk(g_mu);
     g_hybrid.store(enable != 0);
-    g_plans.clear();
     g_epoch.fetch_add(1);
     return VX_OK;
 }
@@ -748,7 +907,6 @@ vx_status vx_fix_wavefront(int wave_m, int wave_n, int mfma_m)
         g_fix_wm.store(0);
         g_fix_wn.store(0);
         g_fix_mi.store(0);
-        g_plans.clear();
         g_epoch.fetch_add(1);
         return VX_OK;
     }
@@ -769,7 +927,13 @@ vx_status vx_fix_wavefront(int wave_m, int wave_n, int mfma_m)
     g_fix_wm.store(wave_m);
     g_fix_wn.store(wave_n);
     g_fix_mi.store(mfma_m);
-    g_plans.clear();
+    g_epoch.fetch_add(1);
+    return VX_OK;
+}
+
+vx_status vx_test_fail_workspace_alloc(int fail)
+{
+    g_fail_ws_alloc.store(fail != 0);
     g_epoch.fetch_add(1);
     return VX_OK;
 }
@@ -804,6 +968,7 @@ vx_status vx_set_workspace(void* ptr, size_t bytes, void* stream)
         w.owned = false;
         g_ws[key] = w;
     }
+    g_ws_epoch.fetch_add(1);
     g_epoch.fetch_add(1);
     return VX_OK;
 }

@@ -77,3 +77,14 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
 
 // grid-level tile order: tile rows walked together (bounded by the tile count)
 int vxi_group_m(int64_t tiles_m, int64_t tiles_n);
+
+// The GEMM entry's argument checks alone (no HIP call); *noop when M, N or
+// batch is 0.
+vx_status vxi_gemm_check(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                         int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, bool* noop);
+// The batched GEMM with a caller-given split-K scratch (arrival counters at
+// `scratch`, ticket_bytes of them, then partial_bytes of fp32 partials):
+// plans only splits that fit, allocates nothing.
+vx_status vxi_gemm_scratch(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype, const void* A,
+                           int64_t sA, const void* B, int64_t sB, void* C, int64_t sC, void* stream,
+                           void* scratch, size_t ticket_bytes, size_t partial_bytes);

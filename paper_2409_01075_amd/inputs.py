@@ -168,13 +168,60 @@ def device_normal(shape, std, seed, device, dtype):
 
 
 def device_softmax_rows(shape, seed, device, dtype):
-    """Seeded row softmax of N(0, 1) logits, drawn on the device (timing runs)."""
+    """Seeded row softmax (binary64) of N(0, 1) logits, drawn on the device
+    (timing runs and full-size parity), rounded to `dtype`."""
     import torch
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
-    z = torch.empty(shape, dtype=torch.float32, device=device)
+    z = torch.empty(shape, dtype=torch.float64, device=device)
     z.normal_(0.0, 1.0, generator=gen)
     return torch.softmax(z, dim=-1).to(dtype)
+
+
+def device_set(name, trials=None):
+    """The GEMMs of a bf16 workload set as drawn for the device runs (timing and
+    full-size parity): a list of (label, batch, M, N, K, make), where make(dev)
+    returns the seeded device operands (A, B) as bf16 torch tensors -- A with
+    batch * M rows of K, B with batch * K rows of N.  Shapes come from the
+    set's seeded draws (encoder_shape, attention_L, llm_M); values from
+    device_normal / device_softmax_rows with seed 1000 t + operand index.
+
+    name: "encoder" (64 trials x 4 GEMMs), "attention" (32 trials x S and O,
+    batch 192) or "llm" (48 trials x 3 GEMMs)."""
+    import torch
+    bf = torch.bfloat16
+    jobs = []
+    if name == "encoder":
+        for t in range(64 if trials is None else trials):
+            M = encoder_shape(t)
+            for gi, (K, N) in enumerate(ENCODER_SHAPES):
+                def mk(dev, t=t, gi=gi, M=M, K=K, N=N):
+                    return (device_normal((M, K), 1.0, 1000 * t + 2 * gi, dev, bf),
+                            device_normal((K, N), 0.02, 1000 * t + 2 * gi + 1, dev, bf))
+                jobs.append(("t%d G%d (%d,%d)x(%d,%d)" % (t, gi + 1, M, K, K, N), 1, M, N, K, mk))
+    elif name == "llm":
+        for t in range(48 if trials is None else trials):
+            M = llm_M(t)
+            for gi, (K, N) in enumerate(LLM_SHAPES):
+                def mk(dev, t=t, gi=gi, M=M, K=K, N=N):
+                    return (device_normal((M, K), 1.0, 1000 * t + 2 * gi, dev, bf),
+                            device_normal((K, N), 0.02, 1000 * t + 2 * gi + 1, dev, bf))
+                jobs.append(("t%d H%d (%d,%d)x(%d,%d)" % (t, gi + 1, M, K, K, N), 1, M, N, K, mk))
+    elif name == "attention":
+        b, d = ATTN_BATCH, ATTN_HEAD
+        for t in range(32 if trials is None else trials):
+            L = attention_L(t)
+            def mk_s(dev, t=t, L=L):
+                return (device_normal((b, L, d), 1.0, 1000 * t, dev, bf),
+                        device_normal((b, d, L), 1.0, 1000 * t + 1, dev, bf))
+            def mk_o(dev, t=t, L=L):
+                return (device_softmax_rows((b, L, L), 1000 * t + 2, dev, bf),
+                        device_normal((b, L, d), 1.0, 1000 * t + 3, dev, bf))
+            jobs.append(("t%d S L=%d" % (t, L), b, L, L, d, mk_s))
+            jobs.append(("t%d O L=%d" % (t, L), b, L, d, L, mk_o))
+    else:
+        raise ValueError("unknown set %r" % name)
+    return jobs
 
 
 def small_int(g, shape, dtype, lo, hi):

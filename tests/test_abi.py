@@ -532,3 +532,19 @@ def test_equal_costs_go_to_fewer_k_slices(mi355x_override):
         best = min(c for c, _ in costs)
         fewest = min(s for c, s in costs if c == best)
         assert p.predicted_ns == best and p.split_k == fewest, ((M, N, K), p.split_k, fewest)
+
+
+def test_workspace_failure_hook_plans_without_split(mi355x_override):
+    """With the library's workspace unavailable, planning returns plans that
+    need none (the fallback a launch takes when the allocation fails)."""
+    M, N, K = 16, 4096, 11008
+    p = vx.vx_plan_query(1, M, N, K, 2)
+    assert p.split_k > 1 and p.workspace_bytes > 0
+    assert vx.vx_test_fail_workspace_alloc(1) == 0
+    try:
+        q = vx.vx_plan_query(1, M, N, K, 2)
+        assert q.split_k == 1 and q.workspace_bytes == 0 and q.dp_tiles == 0
+    finally:
+        vx.vx_test_fail_workspace_alloc(0)
+    r = vx.vx_plan_query(1, M, N, K, 2)
+    assert (r.kernel_id, r.split_k) == (p.kernel_id, p.split_k)

@@ -242,6 +242,27 @@ def test_sampled_matches_full():
     ref, mag = oracle.gemm_sampled(A, B, F16, M, N, K, rows, cols, bats)
     assert np.array_equal(ref, C[bats, rows, cols])
     assert np.array_equal(mag, Mag[bats, rows, cols])
+    # the threaded form (samples grouped by column, columns decoded once per
+    # group) gives the same binary64 values, for any thread count
+    for threads in (2, 3, 8, 500):
+        ref_t, mag_t = oracle.gemm_sampled(A, B, F16, M, N, K, rows, cols, bats, threads=threads)
+        assert np.array_equal(ref_t, ref) and np.array_equal(mag_t, mag)
+
+
+@pytest.mark.parametrize("code", [F32, F16, BF16])
+def test_sampled_threaded_matches_full_bf16_f32_broadcast(code):
+    """Threaded sampling with a broadcast B (sB = 0) and repeated columns."""
+    g = I.rng(51 + code)
+    bt, M, K, N = 3, 17, 65, 23
+    A = I.normal(g, (bt, M, K), code)
+    B = I.normal(g, (K, N), code)
+    C, Mag = oracle.gemm(A, B, code, M=M, N=N, K=K, batch=bt, sB=0)
+    rows = np.concatenate([np.full(N, M - 1), np.arange(M), g.integers(0, M, 300)])
+    cols = np.concatenate([np.arange(N), np.full(M, N - 1), g.integers(0, N, 300)])
+    bats = g.integers(0, bt, rows.size)
+    ref, mag = oracle.gemm_sampled(A, B, code, M, N, K, rows, cols, bats, sB=0, threads=4)
+    assert np.array_equal(ref, C[bats, rows, cols])
+    assert np.array_equal(mag, Mag[bats, rows, cols])
 
 
 def test_threads_do_not_change_results():
