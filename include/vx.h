@@ -146,6 +146,25 @@ vx_status vx_gemm_batched(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dty
                           void* C, int64_t strideC, void* stream);
 
 /*
+ * vx_gemm_batched for callers that cannot allocate device memory: code under
+ * HIP graph capture, serving loops and harnesses that forbid hipMalloc.  Same
+ * arguments, semantics and errors as vx_gemm_batched; the caller still passes
+ * A, B and C.  The split-K scratch (arrival counters and fp32 partial tiles)
+ * is a static device array of 16 MiB + 64 KiB that each GPU the library runs
+ * on holds until the process ends; no call allocates or frees anything.
+ * Plans are chosen among those whose partials fit that array; a plan forced
+ * with vx_force_plan that needs more returns VX_ERR_WORKSPACE.  The first call
+ * on a device clears the array's counters with a small kernel on `stream`
+ * (which a capture records like any kernel); afterwards they reset themselves.
+ * Every call on one GPU shares that GPU's array, so calls that overlap in time
+ * on one GPU (concurrent streams, or graph replays beside eager calls) race
+ * and must be ordered by the caller.
+ */
+vx_status vx_gemm_batched_noalloc(int64_t batch, int64_t M, int64_t N, int64_t K, vx_dtype dtype,
+                                  const void* A, int64_t strideA, const void* B, int64_t strideB,
+                                  void* C, int64_t strideC, void* stream);
+
+/*
  * The plan vx_gemm_batched would use, without launching anything (host only).
  * base_align: the largest power of two dividing the byte addresses of A, B
  * and C (0 means 256).  Strides as for vx_gemm_batched.

@@ -75,6 +75,8 @@ def lib():
     L.vx_gemm.restype = i32
     L.vx_gemm_batched.argtypes = [i64, i64, i64, i64, i32, vp, i64, vp, i64, vp, i64, vp]
     L.vx_gemm_batched.restype = i32
+    L.vx_gemm_batched_noalloc.argtypes = [i64, i64, i64, i64, i32, vp, i64, vp, i64, vp, i64, vp]
+    L.vx_gemm_batched_noalloc.restype = i32
     L.vx_test_fail_workspace_alloc.argtypes = [i32]
     L.vx_test_fail_workspace_alloc.restype = i32
     L.vx_plan_query.argtypes = [i64, i64, i64, i64, i32, i64, i64, i64, ctypes.c_uint64, ctypes.POINTER(vx_plan)]
@@ -141,6 +143,10 @@ def vx_gemm(M, N, K, dtype, A, B, C, stream=None):
 
 def vx_gemm_batched(batch, M, N, K, dtype, A, sA, B, sB, C, sC, stream=None):
     return lib().vx_gemm_batched(batch, M, N, K, dtype, A, sA, B, sB, C, sC, stream)
+
+
+def vx_gemm_batched_noalloc(batch, M, N, K, dtype, A, sA, B, sB, C, sC, stream=None):
+    return lib().vx_gemm_batched_noalloc(batch, M, N, K, dtype, A, sA, B, sB, C, sC, stream)
 
 
 def vx_test_fail_workspace_alloc(fail):
