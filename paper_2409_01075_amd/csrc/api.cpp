@@ -457,6 +457,26 @@ vx_status plan_and_launch(const VxShape& sh, VxGemmArgs a, void* stream, const W
     // rotated K order where one batch entry's operands stay resident in an
     // XCD's L2 (the plain-ring direct-to-LDS kernels read it)
     a.krot = g_krot.load() && (double)(sh.M * sh.K + sh.K * sh.N) * elem_bytes(sh.dt) <= t_hw.l2_bytes_per_xcd ? 1 : 0;
+    // the grid decode's divisors (grid_pos): XCD remap quotients per class of
+    // workgroups and fast-division multipliers
+    {
+        const int nx = t_hw.num_xcd > 0 ? t_hw.num_xcd : 1;
+        const int64_t tiles = plan.tiles_m * plan.tiles_n;
+        const int64_t rest = plan.grid - plan.dp_tiles;   // the plain grid, or the hybrid's split class
+        a.xq = (int)(rest / nx);
+        a.xr = (int)(rest % nx);
+        a.xq_dp = (int)(plan.dp_tiles / nx);
+        a.xr_dp = (int)(plan.dp_tiles % nx);
+        a.f_xcd = vx_fastdiv_make((unsigned)nx);
+        a.f_tiles = vx_fastdiv_make((unsigned)tiles);
+        a.f_split = vx_fastdiv_make((unsigned)plan.split_k);
+        const int64_t rt = sh.batch * tiles - plan.dp_tiles;
+        a.f_rt = vx_fastdiv_make((unsigned)(rt > 0 ? rt : 1));
+        a.f_group = vx_fastdiv_make((unsigned)(plan.group_m * plan.tiles_n));
+        a.f_gm = vx_fastdiv_make((unsigned)plan.group_m);
+        const int64_t last = plan.tiles_m - (plan.tiles_m - 1) / plan.group_m * plan.group_m;
+        a.f_gm_last = vx_fastdiv_make((unsigned)last);
+    }
     a.ws = plan.split_k > 1 ? (float*)(ws.base + ws.ticket_bytes) : nullptr;
     a.tickets = plan.split_k > 1 ? (unsigned*)ws.base : nullptr;
     hipError_t e = reg[plan.kernel_id].launch(&a, plan.grid, (hipStream_t)stream);

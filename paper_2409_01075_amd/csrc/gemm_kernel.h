@@ -485,6 +485,10 @@ __device__ __forceinline__ VxGemmArgs pin_args(const VxGemmArgs& in)
                           "+s"(p.K), "+s"(p.tiles_m), "+s"(p.tiles_n), "+s"(p.split), "+s"(p.k_per_split),
                           "+s"(p.batch), "+s"(p.group_m), "+s"(p.num_xcd), "+s"(p.grid), "+s"(p.dp_tiles),
                           "+s"(p.ws), "+s"(p.tickets));
+    asm volatile("" : "+s"(p.xq), "+s"(p.xr), "+s"(p.xq_dp), "+s"(p.xr_dp), "+s"(p.f_xcd.m), "+s"(p.f_xcd.s),
+                      "+s"(p.f_tiles.m), "+s"(p.f_tiles.s), "+s"(p.f_split.m), "+s"(p.f_split.s), "+s"(p.f_rt.m),
+                      "+s"(p.f_rt.s), "+s"(p.f_group.m), "+s"(p.f_group.s), "+s"(p.f_gm.m), "+s"(p.f_gm.s),
+                      "+s"(p.f_gm_last.m), "+s"(p.f_gm_last.s));
     return p;
 }
 
@@ -504,12 +508,20 @@ struct GridPos {
     int b, z, tm, tn, m0, n0, kbeg, kend, nk, tiles, split, rid;
 };
 
+// x / d for 0 <= x < 2^31, with f = vx_fastdiv_make(d) (see vx_args.h).
+__device__ __forceinline__ int fdiv(int x, VxFastDiv f)
+{
+    return (int)((__umulhi((unsigned)x, f.m) + (unsigned)x) >> f.s);
+}
+
 template <int MB, int NB, int KB>
 __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
 {
     // Workgroups are dispatched round-robin over the XCDs; remap the linear id
     // so that each XCD receives a contiguous range of logical tiles
-    // (neighbouring tiles share A or B panels in that XCD's L2).
+    // (neighbouring tiles share A or B panels in that XCD's L2).  Every
+    // quotient below divides by a launch constant through its host-made
+    // multiplier (fdiv).
     const int w = blockIdx.x;
     const int nx = p.num_xcd;
     GridPos g;
@@ -517,14 +529,14 @@ __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
     int tile;
     bool whole = false;
     if (p.dp_tiles == 0) {
-        // plain grid: every tile in split slices
-        const int G = p.grid;
-        const int xcd = w % nx, q = G / nx, rem = G % nx;
-        const int wl = xcd * q + (xcd < rem ? xcd : rem) + w / nx;
-        tile = wl % g.tiles;
-        const int bz = wl / g.tiles;
-        g.z = bz % p.split;
-        g.b = bz / p.split;
+        // plain grid: every tile in split slices; grid = xq * nx + xr
+        const int wq = fdiv(w, p.f_xcd), xcd = w - wq * nx;
+        const int wl = xcd * p.xq + (xcd < p.xr ? xcd : p.xr) + wq;
+        const int bz = fdiv(wl, p.f_tiles);
+        tile = wl - bz * g.tiles;
+        const int b = fdiv(bz, p.f_split);
+        g.z = bz - b * p.split;
+        g.b = b;
         g.split = p.split;
     } else {
         // hybrid grid: its two classes of workgroups -- the whole tiles
@@ -534,24 +546,28 @@ __device__ __forceinline__ GridPos grid_pos(const VxGemmArgs& p)
         // num_xcd as well
         whole = w < p.dp_tiles;
         const int wc = whole ? w : w - p.dp_tiles;
-        const int G = whole ? p.dp_tiles : p.grid - p.dp_tiles;
-        const int xcd = wc % nx, q = G / nx, rem = G % nx;
-        const int wl = xcd * q + (xcd < rem ? xcd : rem) + wc / nx;
+        const int q = whole ? p.xq_dp : p.xq, rem = whole ? p.xr_dp : p.xr;
+        const int wq = fdiv(wc, p.f_xcd), xcd = wc - wq * nx;
+        const int wl = xcd * q + (xcd < rem ? xcd : rem) + wq;
         const int rt = p.batch * g.tiles - p.dp_tiles;   // tiles that are split
-        const int T = whole ? wl : p.dp_tiles + wl % rt;
-        g.z = whole ? 0 : wl / rt;
-        g.b = T / g.tiles;
-        tile = T % g.tiles;
+        const int zq = fdiv(wl, p.f_rt), rr = wl - zq * rt;
+        const int T = whole ? wl : p.dp_tiles + rr;
+        g.z = whole ? 0 : zq;
+        g.b = fdiv(T, p.f_tiles);
+        tile = T - g.b * g.tiles;
         g.split = whole ? 1 : p.split;
-        g.rid = whole ? 0 : wl % rt;
+        g.rid = whole ? 0 : rr;
     }
     // grouped order: group_m tile rows are walked column by column
     const int per_group = p.group_m * p.tiles_n;
-    const int grp = tile / per_group;
+    const int grp = fdiv(tile, p.f_group);
+    const int r = tile - grp * per_group;
     const int first_m = grp * p.group_m;
-    const int gm = min(p.group_m, p.tiles_m - first_m);
-    g.tm = first_m + (tile % per_group) % gm;
-    g.tn = (tile % per_group) / gm;
+    const bool full = p.tiles_m - first_m >= p.group_m;
+    const int gm = full ? p.group_m : p.tiles_m - first_m;
+    const int tn = fdiv(r, full ? p.f_gm : p.f_gm_last);
+    g.tm = first_m + (r - tn * gm);
+    g.tn = tn;
     g.m0 = g.tm * MB;
     g.n0 = g.tn * NB;
     if (p.dp_tiles == 0)
