@@ -148,6 +148,8 @@ def _shape_for(k, extra_m=3, extra_n=5, extra_k=8):
     M = 2 * k.mb + extra_m
     N = k.nb + (8 if k.align & 2 else extra_n)           # B's rows aligned only where the kernel needs it
     K = 2 * k.kb + (8 if k.align & 1 else extra_k + 1)   # likewise A's
+    if k.k_max and K > k.k_max:                           # a kernel that holds its whole slice
+        K = k.k_max - 8
     return M, N, K
 
 
