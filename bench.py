@@ -21,6 +21,14 @@ time in the sweep: its algorithmic bytes per launch (the compulsory
 8 TB/s HBM peak (every sweep shape is below the fp16 ridge point of 314.6
 FLOP/byte).  cpu_baseline times the CPU oracle on a bounded subset of the
 same shapes on this host's cores.
+
+Beside the sweep the same run reports: launch_floor_us, the back-to-back
+device time of an empty kernel (the dispatch floor every sweep shape sits on:
+their roofline times are 0.15-0.34 us) and k0_call_us, this library's
+smallest launch (a K = 0 call); and "sets", a stated sample of the bf16
+workload sets (encoder trials 0-3, attention trials 0-1, LLM trials 0-5),
+each GEMM timed like --workload runs do, with geomean TFLOP/s and roofline
+fractions split by bound (--no-sets skips it).
 """
 import argparse
 import ctypes
@@ -72,6 +80,9 @@ def _parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--m-max", type=int, default=512, help="sweep M = 1..m_max")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sets", action="store_true",
+                    help="skip the sample of the encoder, attention and LLM sets that the default sweep run "
+                         "also times")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--detail", default=None, help="write per-M results as JSON to this path")
     ap.add_argument("--rot-mib", type=int, default=512,
@@ -131,11 +142,27 @@ def _selector_kind():
 
 
 def _cpu_threads():
+    """Threads for the CPU oracle: the CPUs this process may run on, at most
+    16 (one GPU's share of the host's cores on the measurement machines)."""
+    return max(1, min(16, _affinity_cpus()))
+
+
+def _affinity_cpus():
     try:
-        n = len(os.sched_getaffinity(0))
+        return len(os.sched_getaffinity(0))
     except AttributeError:
-        n = os.cpu_count() or 1
-    return max(1, min(16, n))
+        return os.cpu_count() or 1
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def _cpu_baseline(ms, budget_s):
@@ -158,8 +185,10 @@ def _cpu_baseline(ms, budget_s):
             break
     geo = math.exp(sum(math.log(r) for r in rates) / len(rates))
     return {"value": geo, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "affinity_cpus": _affinity_cpus(), "cpu_model": _cpu_model(),
             "sample": "fp16 sweep shapes M in %s (every 8th M from 1, %d shapes, full outputs, "
-                      "fp64 accumulation, decode included), geomean over the sample"
+                      "fp64 accumulation, decode included), geomean over the sample; threads = the "
+                      "process's CPUs, at most 16 (one GPU's share of the host)"
                       % ("{%d..%d}" % (done[0], done[-1]), len(done))}
 
 
@@ -620,18 +649,16 @@ def run_conv(args):
     print(json.dumps(out), flush=True)
 
 
-def run_set(args):
-    """Times every GEMM of a set over rotating HBM-resident copies and reports
-    TFLOP/s and the fraction of each shape's roofline."""
+def _time_jobs(jobs, rot_mib, dev, compare_torch=False, verbose=True):
+    """Times every GEMM of `jobs` over rotating HBM-resident copies; per GEMM
+    the median of 3 windows of back-to-back calls (a spin ahead of each window
+    lets the host queue the calls first).  Returns one dict per GEMM."""
     import numpy as np
     import torch
     from paper_2409_01075_amd import vx
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     L = vx.lib()
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
-    jobs = _set_jobs(args.workload, args.trials, args.shapes, args.dtype)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     torch.cuda._sleep(1000000)
@@ -643,7 +670,7 @@ def run_set(args):
         eb = 4 if dt == 0 else 2
         A, B = mk(dev)
         set_bytes = b * (M * K + K * N + M * N) * eb
-        R = int(min(max(2, -(-args.rot_mib * 2 ** 20 // set_bytes)), 4096))
+        R = int(min(max(2, -(-rot_mib * 2 ** 20 // set_bytes)), 4096))
         pa = A.reshape(1, -1).expand(R, -1).contiguous()
         pb = B.reshape(1, -1).expand(R, -1).contiguous()
         pc = torch.empty((R, b * M * N), dtype=A.dtype, device=dev)
@@ -663,7 +690,7 @@ def run_set(args):
         n_calls = max(R, 8)
         for _ in range(3):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda._sleep(int(cycles_per_ms * 0.3))
+            torch.cuda._sleep(int(cycles_per_ms * (0.3 + 0.006 * n_calls)))
             e0.record(stream)
             for i in range(n_calls):
                 call(i % R)
@@ -681,7 +708,7 @@ def run_set(args):
              "gbps": bytes_min / t / 1e9, "bound": "mfma" if t_mfma >= t_hbm else "hbm",
              "roof_frac": max(t_mfma, t_hbm) / t, "kernel": plan.kernel_id, "split": plan.split_k,
              "tile": [plan.kernel.mb, plan.kernel.nb, plan.kernel.kb, plan.kernel.stages]}
-        if args.compare_torch:
+        if compare_torch:
             At = A.reshape(b, M, K) if b > 1 else A
             Bt = B.reshape(b, K, N) if b > 1 else B
             torch.matmul(At, Bt)
@@ -694,17 +721,41 @@ def run_set(args):
             torch.cuda.synchronize()
             r["torch_us"] = e0.elapsed_time(e1) / 8 * 1e3
         results.append(r)
-        print("%-34s %9.1f us %8.1f TFLOP/s %7.0f GB/s  %s %5.1f%% of roof  kid %d split %d %s%s"
-              % (label, r["us"], r["tflops"], r["gbps"], r["bound"], 100 * r["roof_frac"], r["kernel"],
-                 r["split"], r["tile"], ("  torch %.1f us" % r["torch_us"]) if "torch_us" in r else ""),
-              file=sys.stderr, flush=True)
+        if verbose:
+            print("%-34s %9.1f us %8.1f TFLOP/s %7.0f GB/s  %s %5.1f%% of roof  kid %d split %d %s%s"
+                  % (label, r["us"], r["tflops"], r["gbps"], r["bound"], 100 * r["roof_frac"], r["kernel"],
+                     r["split"], r["tile"], ("  torch %.1f us" % r["torch_us"]) if "torch_us" in r else ""),
+                  file=sys.stderr, flush=True)
         del pa, pb, pc, A, B
+    return results
 
-    def geo(v):
-        v = [x for x in v if x > 0]
-        return float(np.exp(np.mean(np.log(v)))) if v else None
+
+def _geo(v):
+    import numpy as np
+    v = [x for x in v if x > 0]
+    return float(np.exp(np.mean(np.log(v)))) if v else None
+
+
+def _set_summary(results):
+    """Geomean TFLOP/s and roofline fractions of a timed set, split by bound."""
     hbm = [r for r in results if r["bound"] == "hbm"]
     mf = [r for r in results if r["bound"] == "mfma"]
+    return {"gemms": len(results), "tflops_geomean": _geo([r["tflops"] for r in results]),
+            "roof_frac_geomean": _geo([r["roof_frac"] for r in results]),
+            "hbm_bound": {"n": len(hbm), "gbps_geomean": _geo([r["gbps"] for r in hbm]),
+                          "frac_geomean": _geo([r["roof_frac"] for r in hbm])},
+            "mfma_bound": {"n": len(mf), "tflops_geomean": _geo([r["tflops"] for r in mf]),
+                           "frac_geomean": _geo([r["roof_frac"] for r in mf])}}
+
+
+def run_set(args):
+    """Times every GEMM of a set over rotating HBM-resident copies and reports
+    TFLOP/s and the fraction of each shape's roofline."""
+    import torch
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    jobs = _set_jobs(args.workload, args.trials, args.shapes, args.dtype)
+    results = _time_jobs(jobs, args.rot_mib, dev, args.compare_torch)
     by_kernel = {}
     for r in results:
         by_kernel.setdefault(r["kernel"], []).append(r)
@@ -721,27 +772,67 @@ def run_set(args):
         roof = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak}
     roof.update({"traffic": None, "kernel": "vxk_%d" % kid, "launches": len(dom),
                  "avg_us": dom_t / len(dom) * 1e6})
+    summ = _set_summary(results)
     out = {"metric": "GEMM TFLOP/s geomean over dynamic-M sweep; % of MFMA/HBM roofline on 1 GPU",
-           "value": geo([r["tflops"] for r in results]), "unit": "TFLOP/s", "n_gpus": 1,
+           "value": summ["tflops_geomean"], "unit": "TFLOP/s", "n_gpus": 1,
            "steps": 1, "warmup": 1, "ms_per_step": sum(r["us"] for r in results) / 1e3,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": ("f32" if args.workload == "single" else args.dtype if args.workload == "shapes" else "bf16"),
            "data": "synthetic (seeded, on device)",
            "config": {"workload": args.workload, "gemms": len(results)},
            "roofline": roof,
-           "roof_frac_geomean": geo([r["roof_frac"] for r in results]),
-           "hbm_bound": {"n": len(hbm), "gbps_geomean": geo([r["gbps"] for r in hbm]),
-                         "frac_geomean": geo([r["roof_frac"] for r in hbm])},
-           "mfma_bound": {"n": len(mf), "tflops_geomean": geo([r["tflops"] for r in mf]),
-                          "frac_geomean": geo([r["roof_frac"] for r in mf])}}
+           "roof_frac_geomean": summ["roof_frac_geomean"],
+           "hbm_bound": summ["hbm_bound"], "mfma_bound": summ["mfma_bound"]}
     if args.compare_torch:
-        out["vs_torch_matmul_geomean"] = geo([r["torch_us"] / r["us"] for r in results])
+        out["vs_torch_matmul_geomean"] = _geo([r["torch_us"] / r["us"] for r in results])
     _copy_calibration(args, dev)
     if args.detail:
         with open(args.detail, "w") as f:
             json.dump(results, f)
     out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
+
+
+def _launch_floor_us(stream, reps=3, n=400):
+    """Back-to-back device time of an empty kernel (the dispatch floor), with
+    the host queued ahead: the smallest per-call time any kernel launch on
+    this stream can reach."""
+    import numpy as np
+    import torch
+    out = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(20000000)
+        e0.record(stream)
+        for _ in range(n):
+            torch.cuda._sleep(0)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1) * 1e3 / n)
+    return float(np.median(out))
+
+
+def _k0_call_us(stream, L, reps=3, n=400):
+    """Back-to-back device time of this library's smallest launch: a K = 0
+    call (one 16 x 16 tile of zeros)."""
+    import numpy as np
+    import torch
+    c0 = torch.empty((16, 16), dtype=torch.float16, device="cuda")
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    out = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(20000000)
+        e0.record(stream)
+        for _ in range(n):
+            L.vx_gemm(16, 16, 0, 1, None, None, c0.data_ptr(), sp)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1) * 1e3 / n)
+    return float(np.median(out))
+
+
+SET_SAMPLE = (("encoder", 4), ("attention", 2), ("llm", 6))
 
 
 def main():
@@ -878,6 +969,21 @@ def main():
         torch.cuda.synchronize()
         pass_ms.append(e0.elapsed_time(e1))
 
+    # the dispatch floor beside the sweep (every sweep shape's roofline time is below 5 us)
+    launch_floor = _launch_floor_us(stream)
+    k0_call = _k0_call_us(stream, L)
+
+    # a stated sample of the three bf16 sets, timed like their own runs
+    sets_out = {}
+    if not args.no_sets:
+        for name, trials in SET_SAMPLE:
+            res = _time_jobs(_set_jobs(name, trials), args.rot_mib, dev, verbose=False)
+            summ = _set_summary(res)
+            summ["trials"] = "0..%d" % (trials - 1)
+            sets_out[name] = summ
+            print("set %s trials 0..%d: %.1f TFLOP/s geomean, roofline fraction %.3f"
+                  % (name, trials - 1, summ["tflops_geomean"], summ["roof_frac_geomean"]), file=sys.stderr, flush=True)
+
     _copy_calibration(args, dev)
 
     med = np.median(np.array(per_step), axis=0)        # ms per call, per M
@@ -924,7 +1030,11 @@ def main():
         "host_us_per_call": host_us,
         "pass_ms_back_to_back": float(np.median(pass_ms)),
         "kernels_used": len(by_kernel),
+        "launch_floor_us": launch_floor,
+        "k0_call_us": k0_call,
     }
+    if sets_out:
+        out["sets"] = sets_out
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = _cpu_baseline(ms, args.cpu_seconds)
     if args.detail:
