@@ -286,6 +286,21 @@ vx_status vx_enable_hybrid_grid(int enable);
 vx_status vx_enable_k_rotation(int enable);
 
 /*
+ * The search of Equation 1 is exact but prices only the (kernel, split, grid)
+ * triples that can win: each calibrated kernel first gets a lower bound on
+ * its cost over every split and both grids, and is skipped when that bound
+ * exceeds the best cost already found.  With enable = 1 every triple is
+ * priced instead (the plan is the same; the switch exists so that tests can
+ * check that).  0 (the default) restores the pruned search.  Retires cached
+ * plans.  Process-wide; for tests.
+ */
+vx_status vx_selector_exhaustive(int enable);
+
+/* Number of (kernel, split, grid) triples the calling thread's last search
+ * priced (0 before its first search; a cached plan is not a search). */
+int64_t vx_selector_last_evaluations(void);
+
+/*
  * Test hook for the split-K workspace fallback: with fail != 0 the library's
  * own lazily allocated workspace is treated as unavailable, so calls on a
  * stream without a workspace plan without split-K (as they do when the

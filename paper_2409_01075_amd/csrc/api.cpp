@@ -40,6 +40,7 @@ std::atomic<bool> g_hybrid{true};  // hybrid grids among the plans (vx_enable_hy
 std::atomic<bool> g_krot{true};    // rotated K order in the direct-to-LDS GEMM kernels (vx_enable_k_rotation)
 std::atomic<uint64_t> g_epoch{0};   // bumps when planning inputs change
 std::atomic<bool> g_fail_ws_alloc{false};   // test hook: the lazy workspace allocation fails
+std::atomic<bool> g_exhaustive{false};      // test switch: the search prices every pair
 
 struct PlanKey {
     int64_t batch, M, N, K;
@@ -630,6 +631,10 @@ vx_status conv_shape(const vx_conv2d_desc* d, VxShape* sh, VxGemmArgs* a, bool* 
 
 }  // namespace
 
+uint64_t vxi_plan_epoch(void) { return g_epoch.load(); }
+
+bool vxi_exhaustive_search(void) { return g_exhaustive.load(std::memory_order_relaxed); }
+
 const VxCalib* vxi_calib(int kernel_id)
 {
     if (!g_calib_loaded.load() || !g_calib_enabled.load())
@@ -667,6 +672,14 @@ vx_status vx_calibration_load(const char* path, int* n_loaded)
     if (n_loaded)
         *n_loaded = n > 0 ? n : 0;
     return n > 0 ? VX_OK : VX_ERR_INVALID_ARG;
+}
+
+vx_status vx_selector_exhaustive(int enable)
+{
+    g_exhaustive.store(enable != 0);
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_epoch.fetch_add(1);
+    return VX_OK;
 }
 
 vx_status vx_calibration_enable(int enable)

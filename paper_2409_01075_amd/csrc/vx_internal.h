@@ -29,6 +29,12 @@ const VxCalib* vxi_calib(int kernel_id);
 // Dispatch constant: the calibrated launch floor when loaded, else hw.launch_ns.
 double vxi_calib_launch_ns(const vx_hwinfo& hw);
 
+// Planning epoch: changes whenever a planning input does (calibration,
+// hardware override, ablation switches, workspaces).
+uint64_t vxi_plan_epoch(void);
+// True while the search must price every (kernel, split) pair (a test switch).
+bool vxi_exhaustive_search(void);
+
 // Device description from hipDeviceProp_t plus the per-architecture table.
 // Returns 0 on success.
 int vxi_device_hwinfo(int device, vx_hwinfo* out);

@@ -97,6 +97,10 @@ def lib():
     L.vx_registry_get.restype = i32
     L.vx_enable_hybrid_grid.argtypes = [i32]
     L.vx_enable_hybrid_grid.restype = i32
+    L.vx_selector_exhaustive.argtypes = [i32]
+    L.vx_selector_exhaustive.restype = i32
+    L.vx_selector_last_evaluations.argtypes = []
+    L.vx_selector_last_evaluations.restype = ctypes.c_int64
     L.vx_enable_k_rotation.argtypes = [i32]
     L.vx_enable_k_rotation.restype = i32
     L.vx_force_plan.argtypes = [i32, i32]
@@ -227,6 +231,14 @@ def vx_restrict_backends(mask=0):
 
 def vx_enable_hybrid_grid(enable=1):
     return lib().vx_enable_hybrid_grid(enable)
+
+
+def vx_selector_exhaustive(enable=1):
+    return lib().vx_selector_exhaustive(enable)
+
+
+def vx_selector_last_evaluations():
+    return lib().vx_selector_last_evaluations()
 
 
 def vx_enable_k_rotation(enable=1):
