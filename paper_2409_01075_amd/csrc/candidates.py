@@ -1,18 +1,19 @@
 """Build-time candidate generation (Section 5.1, Algorithm 2) for gfx950.
 
-Runs once, offline, when the library is built: it derives the micro-kernel
-candidates of every level bottom-up from the hardware description, keeping at
-each level only tiles that are integer multiples of a candidate of the level
-below, and records the upper -> lower links.  The surviving workgroup-level
-candidates become the kernel instantiations compiled into the library; the
-runtime selector then chooses among them analytically (Section 5.2).
-
-Levels (Table 1, GPU rows):
-  L0  MFMA instruction tile (m0, n0, k0): filtered by the ISA (FilterByISA).
-  L1  wavefront tile (Mw, Nw): register level, multiples of an L0 tile.
-  L2  workgroup tile (Mb, Nb, Kb) with wm x wn wavefronts: LDS level,
-      multiples of an L1 tile (FilterByMultiples).
-The grid level has no tile of its own: it is the runtime parallel loop.
+Runs once, offline, when the library is built.  Algorithm 2 builds each
+level's candidates as integer multiples of the level below it and links every
+upper tile to the lower tiles it is made of; here the three levels are plain
+functions of the hardware table, each calling the one below:
+  mfma_tiles        L0  instruction tiles (m0, n0, k0) the ISA offers per dtype.
+  wave_tiles        L1  wavefront tiles (Mw, Nw), register level: multiples of
+                        an L0 tile, {wave tile: [its L0 tiles]}.
+  workgroup_tiles   L2  workgroup tiles (Mb, Nb, Kb) with wm x wn wavefronts,
+                        LDS level: multiples of an L1 tile,
+                        {workgroup tile: [(wave tile, L0 tile)]}.
+The grid level has no tile of its own: it is the runtime parallel loop.  The
+workgroup tiles that pass the feasibility rules become the kernel
+instantiations compiled into the library; the runtime selector then chooses
+among them analytically (Section 5.2).
 
 Two level-1 load strategies exist (the Load stage of Algorithm 1 at the
 workgroup level):
@@ -43,7 +44,6 @@ this library's reading):
     else the 16 x 16 MFMA.  The paper takes this decision by profiling L0
     offline; until such a calibration exists this fixed rule stands in.
 """
-import itertools
 import json
 import sys
 
@@ -65,43 +65,6 @@ LDS_RESERVE = 1024   # the split-K arrival flag and alignment share the CU's LDS
 ELEM_BYTES = {"f32": 4, "f16": 2, "bf16": 2}
 
 
-def get_hardware_info(level, hw=GFX950):
-    return hw
-
-
-# ------------------------------------------------------------------ L0 -----
-def init_cands_l0(hw):
-    dims = [4, 8, 16, 32, 64]
-    ks = [1, 2, 4, 8, 16, 32, 64]
-    return [(m, n, k) for m in dims for n in dims for k in ks]
-
-
-def filter_by_isa(cands, dtype, hw):
-    legal = set(hw["mfma"][dtype])
-    return [c for c in cands if c in legal]
-
-
-# ------------------------------------------------------------------ L1 -----
-def init_cands_l1(hw, family="reg"):
-    # accumulator budget: register-staged tiles keep up to 128 VGPRs for the
-    # staging registers; direct-to-LDS tiles stage nothing in VGPRs and may
-    # hold 256 fp32 accumulators per lane (the AGPR half of the file)
-    acc_max = 256 if family == "dma" else 128
-    out = []
-    for mw in (16, 32, 64, 128, 256):
-        for nw in (16, 32, 64, 128, 256):
-            acc = mw * nw // hw["wave"]
-            if 4 <= acc <= acc_max and max(mw, nw) <= 4 * min(mw, nw):
-                out.append((mw, nw))
-    return out
-
-
-def multiples_l1(prev, cands):
-    m0, n0, _ = prev
-    return [c for c in cands if c[0] % m0 == 0 and c[1] % n0 == 0]
-
-
-# ------------------------------------------------------------------ L2 -----
 WAVE_GRIDS = [(1, 1), (1, 2), (2, 1), (2, 2), (1, 4), (4, 1), (2, 4), (4, 2)]
 
 
@@ -185,45 +148,60 @@ def feasible_l2(dtype, mb, nb, kb, wm, wn, mi, hw, family):
     return True
 
 
-def generate_candidates_for_layer(level, dtype, hw=GFX950, family=None):
-    """Algorithm 2: returns (cands, link) for `level`; link maps a candidate
-    to the list of lower-level candidates it is an integer multiple of."""
-    hw = get_hardware_info(level, hw)
-    if level == 0:
-        return filter_by_isa(init_cands_l0(hw), dtype, hw), {}
+# ------------------------------------------------------------ the levels -----
+def mfma_tiles(dtype, hw=GFX950):
+    """Level 0: the matrix-core instruction tiles (m, n, k) with fp32
+    accumulation that the ISA offers for `dtype`."""
+    return list(hw["mfma"][dtype])
+
+
+def wave_tiles(dtype, hw=GFX950, family="reg"):
+    """Level 1: wavefront tiles (Mw, Nw) that are integer multiples of at least
+    one level-0 tile, with Mw * Nw / 64 fp32 accumulators per lane within the
+    family's budget (register-staged tiles keep up to 128 VGPRs for their
+    staging registers; direct-to-LDS tiles stage nothing in VGPRs and may use
+    256, the AGPR half of the file) and an aspect of at most 4.
+    Returns {wave tile: [the level-0 tiles it is a multiple of]}."""
+    acc_max = 256 if family == "dma" else 128
+    out = {}
+    for mw in (16, 32, 64, 128, 256):
+        for nw in (16, 32, 64, 128, 256):
+            acc = mw * nw // hw["wave"]
+            if not (4 <= acc <= acc_max and max(mw, nw) <= 4 * min(mw, nw)):
+                continue
+            below = [t for t in mfma_tiles(dtype, hw) if mw % t[0] == 0 and nw % t[1] == 0]
+            if below:
+                out[(mw, nw)] = below
+    return out
+
+
+def mfma_for(mw, nw):
+    """The instruction tile a wavefront tile is built from: 32 x 32 when both
+    sides are multiples of 32 and at least 64 (half the fragment loads per
+    FLOP of 16 x 16), else 16 x 16."""
+    return 32 if (mw % 32 == 0 and nw % 32 == 0 and min(mw, nw) >= 64) else 16
+
+
+def workgroup_tiles(dtype, hw=GFX950, family=None):
+    """Level 2: workgroup tiles (Mb, Nb, Kb, wm, wn, mi) = (wm Mw, wn Nw, Kb) for
+    every wavefront tile (Mw, Nw) and wavefront grid (wm, wn), with Kb a
+    multiple of the instruction's k, that pass the feasibility rules of the
+    family (feasible_l2).  Returns {workgroup tile: [(wave tile, mfma tile)]}."""
     if family is None:
         family = "dma" if ELEM_BYTES[dtype] == 2 else "reg"
-    prev, _ = generate_candidates_for_layer(level - 1, dtype, hw, family)
-    cands, link = [], {}
-    if level == 1:
-        init = init_cands_l1(hw, family)
-        for p in prev:
-            for c in multiples_l1(p, init):
-                if c not in link:
-                    cands.append(c)
-                    link[c] = []
-                link[c].append(p)
-        return cands, link
-    if level == 2:
-        l1_links = generate_candidates_for_layer(1, dtype, hw, family)[1]
-        kbs = (64, 128, 256) if ELEM_BYTES[dtype] == 2 else (32, 64)
-        for (mw, nw) in prev:
-            for (wm, wn) in WAVE_GRIDS:
-                for kb in kbs:
-                    for l0 in l1_links[(mw, nw)]:
-                        mi = l0[0]
-                        want = 32 if (mw % 32 == 0 and nw % 32 == 0 and min(mw, nw) >= 64) else 16
-                        if mi != want or kb % l0[2]:
-                            continue
-                        c = (wm * mw, wn * nw, kb, wm, wn, mi)
-                        if not feasible_l2(dtype, *c, hw, family):
-                            continue
-                        if c not in link:
-                            cands.append(c)
-                            link[c] = []
-                        link[c].append(((mw, nw), l0))
-        return cands, link
-    raise ValueError("gfx950 GEMM has levels 0..2")
+    kbs = (64, 128, 256) if ELEM_BYTES[dtype] == 2 else (32, 64)
+    out = {}
+    for (mw, nw), below in wave_tiles(dtype, hw, family).items():
+        for (wm, wn) in WAVE_GRIDS:
+            for kb in kbs:
+                for l0 in below:
+                    if l0[0] != mfma_for(mw, nw) or kb % l0[2]:
+                        continue
+                    c = (wm * mw, wn * nw, kb, wm, wn, l0[0])
+                    if not feasible_l2(dtype, *c, hw, family):
+                        continue
+                    out.setdefault(c, []).append(((mw, nw), l0))
+    return out
 
 
 # fp16/bf16 register-staged vector-load tiles kept for operands whose byte
@@ -248,8 +226,7 @@ def dma_wide_candidates(dtype, hw=GFX950):
             acc = mw * nw // hw["wave"]
             if mw % 16 or nw % 16 or not (4 <= acc <= 256) or max(mw, nw) > 4 * min(mw, nw):
                 continue
-            mi = 32 if (mw % 32 == 0 and nw % 32 == 0 and min(mw, nw) >= 64) else 16
-            c = (mb, nb, 64, wm, wn, mi)
+            c = (mb, nb, 64, wm, wn, mfma_for(mw, nw))
             for st in dma_stage_options(*c, 1, hw):
                 out.append(_entry(dtype, "dma", st, c, 1, hw))
     return out
@@ -276,7 +253,7 @@ CONV_TILES = {(32, 32), (32, 64), (64, 32), (64, 64), (64, 128), (128, 64), (128
 def conv_candidates(dtype, hw=GFX950):
     kb = 64 if ELEM_BYTES[dtype] == 2 else 32
     out = []
-    for c in generate_candidates_for_layer(2, dtype, hw, "reg")[0]:
+    for c in workgroup_tiles(dtype, hw, "reg"):
         mb, nb, ckb, wm, wn, mi = c
         if ckb == kb and (mb, nb) in CONV_TILES and wm * wn == 4:
             e = _entry(dtype, "reg", 2, c, 0, hw)
@@ -295,7 +272,7 @@ def conv_candidates(dtype, hw=GFX950):
 # the deepest ring of at most 4 stages.
 def conv_dma_candidates(dtype, hw=GFX950):
     out = []
-    for c in generate_candidates_for_layer(2, dtype, hw, "dma")[0]:
+    for c in workgroup_tiles(dtype, hw, "dma"):
         mb, nb, kb, wm, wn, mi = c
         mw, nw = mb // wm, nb // wn
         if kb != 64 or min(mb, nb) < 64 or mb * nb > 256 * 128 or wm * wn != (8 if mb * nb >= 128 * 128 else 4):
@@ -408,14 +385,14 @@ def registry(hw=GFX950):
     element-aligned operands."""
     out = []
     for dtype in ("f16", "bf16"):
-        for c in generate_candidates_for_layer(2, dtype, hw, "dma")[0]:
+        for c in workgroup_tiles(dtype, hw, "dma"):
             for st in dma_stage_options(*c, 1, hw):
                 out.append(_entry(dtype, "dma", st, c, 1, hw))
-        for c in generate_candidates_for_layer(2, dtype, hw, "reg")[0]:
+        for c in workgroup_tiles(dtype, hw, "reg"):
             out.append(_entry(dtype, "reg", 2, c, 0, hw))
         for c in REG_FALLBACK_16:
             out.append(_entry(dtype, "reg", 2, c, 1, hw))
-    for c in generate_candidates_for_layer(2, "f32", hw, "reg")[0]:
+    for c in workgroup_tiles("f32", hw, "reg"):
         for vec in (1, 0):
             out.append(_entry("f32", "reg", 2, c, vec, hw))
     for dtype in ("f16", "bf16", "f32"):
@@ -436,8 +413,7 @@ def registry(hw=GFX950):
 if __name__ == "__main__":
     reg = registry()
     for dt in ("f16", "bf16", "f32"):
-        for lv in (0, 1, 2):
-            c, _ = generate_candidates_for_layer(lv, dt)
-            print(dt, "L%d" % lv, len(c), file=sys.stderr)
+        print(dt, "L0", len(mfma_tiles(dt)), "L1", len(wave_tiles(dt)), "L2", len(workgroup_tiles(dt)),
+              file=sys.stderr)
     print(len(reg), file=sys.stderr)
     json.dump(reg, sys.stdout, indent=0)

@@ -194,19 +194,29 @@ def test_candidate_generator_properties():
     finally:
         sys.path.pop(0)
     for dt in ("f16", "bf16", "f32"):
-        l0, _ = C.generate_candidates_for_layer(0, dt)
+        l0 = C.mfma_tiles(dt)
         assert set(l0) == set(C.GFX950["mfma"][dt])
-        l1, link1 = C.generate_candidates_for_layer(1, dt)
-        for c in l1:
-            assert link1[c] and all(c[0] % p[0] == 0 and c[1] % p[1] == 0 for p in link1[c])
-            assert 4 <= c[0] * c[1] // 64 <= (256 if dt != "f32" else 128)
-        l2, link2 = C.generate_candidates_for_layer(2, dt)
-        for c in l2:
-            mb, nb, kb, wm, wn, mi = c
-            for (w, l0c) in link2[c]:
-                assert w in l1 and mb == wm * w[0] and nb == wn * w[1]
-                assert kb % l0c[2] == 0 and l0c in l0
-            assert C.lds_bytes(dt, mb, nb, kb) <= C.GFX950["lds_bytes"]
+        for fam in ("reg", "dma"):
+            l1 = C.wave_tiles(dt, family=fam)
+            for c, below in l1.items():
+                assert below and all(c[0] % p[0] == 0 and c[1] % p[1] == 0 for p in below)
+                assert set(below) <= set(l0)
+                assert 4 <= c[0] * c[1] // 64 <= (256 if fam == "dma" else 128)
+            # every multiple of an L0 tile within the budget is present (nothing dropped)
+            for mw in (16, 32, 64, 128):
+                for nw in (16, 32, 64, 128):
+                    if 4 <= mw * nw // 64 <= 128 and max(mw, nw) <= 4 * min(mw, nw):
+                        assert (mw, nw) in l1
+            if fam == "dma" and dt == "f32":
+                continue
+            l2 = C.workgroup_tiles(dt, family=fam)
+            assert l2
+            for c, links in l2.items():
+                mb, nb, kb, wm, wn, mi = c
+                for (w, l0c) in links:
+                    assert w in l1 and mb == wm * w[0] and nb == wn * w[1]
+                    assert kb % l0c[2] == 0 and l0c in l0 and l0c[0] == mi
+                assert C.lds_bytes(dt, mb, nb, kb) <= C.GFX950["lds_bytes"]
     reg = C.registry()
     assert len(reg) == vx.vx_registry_count()
 
