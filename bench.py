@@ -59,6 +59,9 @@ def _parse():
     ap.add_argument("--dtype", default="bf16", choices=["f32", "f16", "bf16"],
                     help="element type for --workload shapes")
     ap.add_argument("--trials", type=int, default=None, help="trials of a GEMM set (default: the full set)")
+    ap.add_argument("--conv-cin", default="models", choices=["models", "plain"],
+                    help="convolution set: channel counts as CNN layers have them (3 or a multiple of 8), "
+                         "or Cin drawn over the whole range 3..832")
     ap.add_argument("--adapt", action="store_true",
                     help="hardware-adaptation study (Section 7.4): fp16, N in {1024, 2048, 4096}, K = 1024, "
                          "M = 1..16, with the matrix-core kernels only, the vector-ALU kernels only, and both")
@@ -551,7 +554,7 @@ def run_conv(args):
     f16 = torch.float16
     results = []
     for t in range(40 if args.trials is None else args.trials):
-        Nb, H, W, Cin, Cout, F, st, pd = I.conv_trial(t)
+        Nb, H, W, Cin, Cout, F, st, pd = I.conv_trial(t, args.conv_cin)
         d = vx.conv_desc(Nb, H, W, Cin, Cout, F, F, vx.VX_F16, (st, st), (pd, pd))
         OH = (H + 2 * pd - F) // st + 1
         OW = (W + 2 * pd - F) // st + 1
@@ -638,8 +641,15 @@ def run_conv(args):
            "warmup": 1, "ms_per_step": sum(r["us"] for r in results) / 1e3, "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic (seeded, on device)",
            "config": {"workload": "dynamic-shape convolution set: fp16 NHWC layers of the CNN ranges of Table 4",
-                      "layers": len(results)},
+                      "layers": len(results), "cin": args.conv_cin},
            "roofline": roof, "roof_frac_geomean": geo([r["roof_frac"] for r in results])}
+    # Cin decides the load family: rows of 8 fp16 channels are 16-byte aligned
+    # (direct-to-LDS im2col), other counts go through the register-staged path.
+    out["by_cin"] = {}
+    for name, sel in (("multiple_of_8", lambda c: c % 8 == 0), ("other", lambda c: c % 8 != 0)):
+        grp = [r for r in results if sel(r["layer"][3])]
+        out["by_cin"][name] = {"layers": len(grp), "tflops_geomean": geo([r["tflops"] for r in grp]),
+                               "roof_frac_geomean": geo([r["roof_frac"] for r in grp])}
     if args.compare_torch:
         out["vs_torch_conv2d_geomean"] = geo([r["torch_us"] / r["us"] for r in results])
     if args.detail:

@@ -35,6 +35,8 @@ sizes listed below; the paper's own benchmark items are not reproduced):
   round(e^U[ln 4, ln 768]) and batch round(e^U[0, ln 64]), halved (batch
   first, then the map) until the layer holds at most 2^25 input and 2^25
   output elements and 4e11 flops.  Images N(0, 1), filters N(0, 0.05).
+  ``conv_trial(t, "plain")`` keeps every dimension but draws
+  Cin = round(e^U[ln 3, ln 832]) (seed 9000 + t): mostly not a multiple of 8.
 * ``small_int`` helpers: integer-valued operands whose every partial sum is
   exact in fp32 and whose result is exact in the output type.
 """
@@ -238,13 +240,20 @@ def exact_range(K, dtype):
     return max(r, 0)
 
 
-def conv_trial(t):
+def conv_trial(t, cin="models"):
     """(N, H, W, Cin, Cout, F, stride, pad) of convolution trial t (fp16, square
-    filter and map, dilation 1)."""
+    filter and map, dilation 1).  cin="models": channel counts as CNN layers
+    have them (3 for a stem, else a multiple of 8); cin="plain": Cin drawn
+    log-uniformly over the whole range 3..832 from a stream of its own (seed
+    9000 + t), every other dimension as in "models"."""
     g = rng(5000 + t)
     F = int(g.choice(CONV_FILTERS, p=CONV_FILTER_P))
     stem = F >= 7 and g.random() < 0.5
     Cin = 3 if stem else 8 * int(round(np.exp(g.uniform(np.log(2), np.log(104)))))
+    if cin == "plain":
+        Cin = int(round(np.exp(rng(9000 + t).uniform(np.log(3), np.log(832)))))
+    elif cin != "models":
+        raise ValueError("cin must be 'models' or 'plain'")
     Cout = 16 * int(round(np.exp(g.uniform(0.0, np.log(32)))))
     stride = (4 if F == 11 else 2) if (stem or g.random() < 0.25) else 1
     pad = F // 2
