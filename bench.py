@@ -659,10 +659,41 @@ def run_conv(args):
     print(json.dumps(out), flush=True)
 
 
+def _device_warmup(dev, ms=150.0):
+    """About `ms` of back-to-back bf16 4096^3 GEMMs through the library before
+    a set is timed: under sustained load the device takes tens of
+    milliseconds to reach its loaded clock, and the first large GEMMs of a
+    process otherwise run up to a fifth slower than the same calls later."""
+    import torch
+    from paper_2409_01075_amd import vx
+    L = vx.lib()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    n = 4096
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    a = torch.randn((n, n), generator=g, device=dev).to(torch.bfloat16)
+    b = torch.randn((n, n), generator=g, device=dev).to(torch.bfloat16)
+    c = torch.empty((n, n), dtype=torch.bfloat16, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    st = L.vx_gemm(n, n, n, vx.VX_BF16, a.data_ptr(), b.data_ptr(), c.data_ptr(), sp)
+    e1.record(stream)
+    if st != 0:
+        raise RuntimeError("warm-up GEMM: %s" % vx.STATUS.get(st, st))
+    torch.cuda.synchronize()
+    for _ in range(int(min(2000, ms / max(e0.elapsed_time(e1), 1e-3)))):
+        L.vx_gemm(n, n, n, vx.VX_BF16, a.data_ptr(), b.data_ptr(), c.data_ptr(), sp)
+    torch.cuda.synchronize()
+    del a, b, c
+
+
 def _time_jobs(jobs, rot_mib, dev, compare_torch=False, verbose=True):
     """Times every GEMM of `jobs` over rotating HBM-resident copies; per GEMM
     the median of 3 windows of back-to-back calls (a spin ahead of each window
-    lets the host queue the calls first).  Returns one dict per GEMM."""
+    lets the host queue the calls first; about 1 ms of untimed calls between
+    the spin and the window brings the clock to its loaded level).  Returns
+    one dict per GEMM."""
     import numpy as np
     import torch
     from paper_2409_01075_amd import vx
@@ -692,15 +723,24 @@ def _time_jobs(jobs, rot_mib, dev, compare_torch=False, verbose=True):
                 return L.vx_gemm(M, N, K, dt, a0 + r * sa, b0 + r * sb, c0 + r * sc, sp)
             return L.vx_gemm_batched(b, M, N, K, dt, a0 + r * sa, M * K, b0 + r * sb, K * N, c0 + r * sc,
                                      M * N, sp)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
         st = call(0)
+        e1.record(stream)
         if st != 0:
             raise RuntimeError("%s: %s" % (label, vx.STATUS.get(st, st)))
         torch.cuda.synchronize()
+        # warm-up: about 1 ms of the same calls between the spin and the timed
+        # window (at most 64), so that a long MFMA-bound window starts at the
+        # clock it runs at in steady state rather than ramping up from idle
+        n_warm = int(min(64, -(-1.0 // max(e0.elapsed_time(e1), 1e-3))))
         times = []
         n_calls = max(R, 8)
         for _ in range(3):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda._sleep(int(cycles_per_ms * (0.3 + 0.006 * n_calls)))
+            torch.cuda._sleep(int(cycles_per_ms * (0.3 + 0.006 * (n_calls + n_warm))))
+            for i in range(n_warm):
+                call((n_calls + i) % R)
             e0.record(stream)
             for i in range(n_calls):
                 call(i % R)
@@ -765,6 +805,7 @@ def run_set(args):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     jobs = _set_jobs(args.workload, args.trials, args.shapes, args.dtype)
+    _device_warmup(dev)
     results = _time_jobs(jobs, args.rot_mib, dev, args.compare_torch)
     by_kernel = {}
     for r in results:
@@ -986,6 +1027,7 @@ def main():
     # a stated sample of the three bf16 sets, timed like their own runs
     sets_out = {}
     if not args.no_sets:
+        _device_warmup(dev)
         for name, trials in SET_SAMPLE:
             res = _time_jobs(_set_jobs(name, trials), args.rot_mib, dev, verbose=False)
             summ = _set_summary(res)
