@@ -28,7 +28,7 @@
 // LDS layouts (dense, 16-byte chunks XOR-swizzled against bank conflicts):
 //   As[m][k]  Mb x Kb, k contiguous   (chunk c of row m stored at c ^ swzA(m))
 //   Bs[k][n]  Kb x Nb, n contiguous   (chunk c of row k stored at c ^ swzB(k);
-//                                     rotated by swzB(k) in rows of 24 chunks)
+//                                     within groups of 8 chunks in rows of 24)
 // B stays in its natural n-contiguous layout; the MFMA fragments of B are
 // read with the transposing LDS read: in each 16-lane group, source lane s
 // points at Bs[k0 + s/4][n0 + 4*(s%4)], and output lane j receives
@@ -100,28 +100,63 @@ struct DCfg {
                   "ping-pong: 8 waves, a 2-stage ring, K steps split evenly over 4 issuing waves");
 };
 
-__device__ __forceinline__ int swz_a(int r, int period) { return r & (period - 1); }
-// B rows hold CPB 16-byte chunks.  With CPB a power of two, logical chunk c
-// of row k sits at position c ^ s(k), s(k) = 2 (k mod 4) mod CPB (an XOR is
-// its own inverse).  Rows of 24 chunks (tiles 192 wide) rotate instead:
-// chunk c at position (c + s(k)) mod CPB.
-template <int CPB>
-__device__ __forceinline__ int swz_b(int k) { return (CPB & (CPB - 1)) == 0 ? (2 * (k & 3)) & (CPB - 1) : (2 * (k & 3)) % CPB; }
-template <int CPB>
+// The LDS serves 16-byte reads 16 lanes per pass and the transposing 8-byte
+// reads 32 lanes per pass, each pass over a 256-byte window of banks; a
+// fragment read is conflict-free when the lanes of one pass cover distinct
+// 16-byte slots of that window.  The swizzles below place the chunks so.
+//
+// A rows hold CPA 16-byte chunks; chunk c of row m sits at c ^ swz_a(m).  An
+// A fragment read takes one chunk from each of 16 consecutive rows: with
+// 128-byte rows (CPA 8) two rows share a window, so the XOR runs over pairs
+// of rows; with 256 bytes and more each row fills the window.  Convolution
+// tiles keep a period of 8 rows, which their im2col DMA addressing assumes.
+template <class C>
+__device__ __forceinline__ int swz_a(int m)
+{
+    if constexpr (C::CONV)
+        return m & 7;
+    else if constexpr (C::CPA == 8)
+        return (m >> 1) & 7;
+    else
+        return m & (C::SWA - 1);
+}
+// B rows hold CPB 16-byte chunks; logical chunk c of row k sits at position
+// c ^ s(k) (an XOR is its own inverse), and in rows of 24 chunks (tiles 192
+// wide) the XOR acts inside aligned groups of 8 chunks.  A pass of the
+// transposing read covers 4 rows x 4 chunks (32 x 32 MFMA: rows k0..k0+3, 32
+// columns) or 8 rows x 2 chunks (16 x 16 MFMA: rows k0..k0+3 and
+// k0+8..k0+11, 16 columns); s(k) spreads those over the 16 slots of the
+// window for each row width (rows 16 columns wide, 2 chunks, cannot be).
+template <int CPB, int MI>
+__device__ __forceinline__ int swz_b(int k)
+{
+    if constexpr ((CPB & (CPB - 1)) != 0)
+        return swz_b<8, MI>(k);
+    else if constexpr (MI == 32 && CPB >= 16)
+        return 4 * (k & 3);
+    else if constexpr (MI == 32 && CPB == 8)
+        return 4 * ((k >> 1) & 1);
+    else if constexpr (MI == 16 && CPB >= 16)
+        return 2 * (k & 3) + 8 * ((k >> 3) & 1);
+    else if constexpr (MI == 16 && CPB == 8)
+        return 2 * ((k >> 1) & 1) + 4 * ((k >> 3) & 1);
+    else if constexpr (MI == 16 && CPB == 4)
+        return 2 * ((k >> 3) & 1);
+    else
+        return (2 * (k & 3)) & (CPB - 1);
+}
+template <int CPB, int MI>
 __device__ __forceinline__ int b_pos(int c, int k)   // LDS position of logical chunk c of row k
 {
     if constexpr ((CPB & (CPB - 1)) == 0)
-        return c ^ swz_b<CPB>(k);
+        return c ^ swz_b<CPB, MI>(k);
     else
-        return (c + swz_b<CPB>(k)) % CPB;
+        return (c & ~7) | ((c & 7) ^ swz_b<CPB, MI>(k));
 }
-template <int CPB>
+template <int CPB, int MI>
 __device__ __forceinline__ int b_chunk(int pos, int k)   // logical chunk held at LDS position pos of row k
 {
-    if constexpr ((CPB & (CPB - 1)) == 0)
-        return pos ^ swz_b<CPB>(k);
-    else
-        return (pos + CPB - swz_b<CPB>(k)) % CPB;
+    return b_pos<CPB, MI>(pos, k);
 }
 
 // s_waitcnt vmcnt(n) for a compile-time n (expcnt and lgkmcnt left at max).
@@ -291,14 +326,14 @@ struct DmaTile {
             // A: rows of the workgroup's panel
             const int instr = wave * A_IPW + I;
             const int slot = instr * 64 + lane;                  // chunk index in the stage
-            const int r = slot / C::CPA, c = (slot % C::CPA) ^ swz_a(r, C::SWA);
+            const int r = slot / C::CPA, c = (slot % C::CPA) ^ swz_a<C>(r);
             const bool ok = r < Mrel && c * 8 < kv;
             dma_lds<C::LANE_BYTES>(ra, stage + instr * C::WAVE_BYTES, ok ? (unsigned)((r * K + c * 8) * 2) : kOOB);
         } else {
             // B: rows k0.. of the batch's B, columns from n0
             const int instr = wave * B_IPW + (I - A_IPW);
             const int slot = instr * 64 + lane;
-            const int k = slot / C::CPB, c = b_chunk<C::CPB>(slot % C::CPB, k);
+            const int k = slot / C::CPB, c = b_chunk<C::CPB, C::MI>(slot % C::CPB, k);
             const bool ok = k < kv && c * 8 < nv;
             dma_lds<C::LANE_BYTES>(rb, stage + C::A_BYTES + instr * C::WAVE_BYTES,
                                    ok ? (unsigned)((k * N + c * 8) * 2) : kOOB);
@@ -376,10 +411,10 @@ struct VgOperand {
             lds_char* dst;
             if constexpr (C::VG == 1) {
                 const int rr = idx / C::CPA, c = idx % C::CPA;
-                dst = stage + rr * (C::KB * 2) + ((c ^ swz_a(rr, C::SWA)) << 4);
+                dst = stage + rr * (C::KB * 2) + ((c ^ swz_a<C>(rr)) << 4);
             } else {
                 const int kk = idx / C::CPB, c = idx % C::CPB;
-                dst = stage + C::A_BYTES + kk * (C::NB * 2) + (b_pos<C::CPB>(c, kk) << 4);
+                dst = stage + C::A_BYTES + kk * (C::NB * 2) + (b_pos<C::CPB, C::MI>(c, kk) << 4);
             }
             *(lds_u32x4*)dst = r[v];
         }
@@ -403,15 +438,15 @@ __device__ __forceinline__ void dma_frags(lds_char* stage, u32x4 (&fa)[C::FM], u
 #pragma unroll
     for (int fm = 0; fm < C::FM; ++fm) {
         const int m = wm0 + fm * C::MI + li;
-        const int c = (kk * (C::KI / 8) + lg) ^ swz_a(m, C::SWA);
+        const int c = (kk * (C::KI / 8) + lg) ^ swz_a<C>(m);
         fa[fm] = *(lds_u32x4*)(As + m * (C::KB * 2) + c * 16);
     }
 #pragma unroll
     for (int fn = 0; fn < C::FN; ++fn) {
         const int n = wn0 + fn * C::MI + tr_n;
         const int k1 = kk * C::KI + tr_k, k2 = k1 + 4;
-        lds_char* p1 = Bs + k1 * (C::NB * 2) + (b_pos<C::CPB>(n >> 3, k1) << 4) + (n & 7) * 2;
-        lds_char* p2 = Bs + k2 * (C::NB * 2) + (b_pos<C::CPB>(n >> 3, k2) << 4) + (n & 7) * 2;
+        lds_char* p1 = Bs + k1 * (C::NB * 2) + (b_pos<C::CPB, C::MI>(n >> 3, k1) << 4) + (n & 7) * 2;
+        lds_char* p2 = Bs + k2 * (C::NB * 2) + (b_pos<C::CPB, C::MI>(n >> 3, k2) << 4) + (n & 7) * 2;
         const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p1);
         const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p2);
         const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
