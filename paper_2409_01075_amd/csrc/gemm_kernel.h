@@ -234,9 +234,24 @@ struct Tile {
                 }
             }
         }
+        // With unit dilation along the width, the KW x Cin elements of one filter
+        // row are contiguous in the NHWC image (k = kw Cin + ci maps to kw Cin + ci
+        // elements past the row's first tap): a chunk that stays within one filter
+        // row, below kend, whose first and last taps fall inside the image, is one
+        // 16-byte (unaligned) load.  The chunk's first tap is at column ca.kw, its
+        // last at kw_last (same row ca.kh).
+        const int run = p.cKW * p.cC;                  // elements of one filter row
+        const int j0 = ca.kw * p.cC + ca.ci;           // the chunk's first element within its row
+        const bool one_row = p.cdw == 1 && j0 + C::VE <= run && ca.gk + C::VE <= kend;
+        const int kw_last = (j0 + C::VE - 1) / p.cC;
 #pragma unroll
         for (int v = 0; v < C::AV; ++v) {
             unsigned e16[C::VE];
+            if (one_row && (unsigned)(ca.ih0[v] + dhe[0]) < (unsigned)p.cH && ca.iw0[v] + dwe[0] >= 0 &&
+                ca.iw0[v] + kw_last < p.cW) {
+                ra[v] = *(const u32x4_u*)(X + (ca.pix[v] + koff[0]) * C::EB);
+                continue;
+            }
 #pragma unroll
             for (int e = 0; e < C::VE; ++e) {
                 unsigned val = 0u;
