@@ -70,6 +70,33 @@ def test_every_conv_kernel_integer_exact(code):
 
 
 @pytest.mark.parametrize("code", DTS)
+def test_every_register_conv_kernel_contiguous_taps(code):
+    """The register-staged convolution kernels with channel counts that are not
+    multiples of the 16-byte chunk and unit dilation along the width: chunks
+    that stay inside one filter row load as one vector, chunks across a filter
+    row's end, on padding or past K are gathered element by element.  A 3 x 5
+    filter with c_in 3, 5 and 12 puts chunk boundaries at every position of a
+    row; small integers make every result exact."""
+    g = I.rng(1250 + code)
+    ks = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count()))
+          if k.op == 1 and k.dtype == code and k.enabled and not k.vec]
+    assert ks
+    for k in ks:
+        for Cin in (3, 5, 12):
+            Cout = k.nb + 5
+            N, H, W, KH, KW, st, pd, dl = 2, 11, 13, 3, 5, (1, 2), (2, 1), (2, 1)
+            x = I.small_int(g, (N, H, W, Cin), code, -3, 3)
+            w = I.small_int(g, (KH, KW, Cin, Cout), code, -3, 3)
+            assert vx.vx_force_plan(k.id, 1) == 0
+            try:
+                y = run_conv(x, w, code, st, pd, dl)
+            finally:
+                vx.vx_force_plan(-1, 0)
+            ref = oracle.conv2d(x, w, code, st, pd, dl, with_mag=False)
+            tolerance.check_exact(y, ref, code, "conv kernel %d Cin %d, unit width dilation" % (k.id, Cin))
+
+
+@pytest.mark.parametrize("code", DTS)
 def test_conv_split_k_integer_exact(code):
     g = I.rng(1300 + code)
     conv = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count()))
