@@ -371,8 +371,8 @@ struct VgOperand {
         u32x4 x = {0, 0, 0, 0};
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
-            const unsigned lo = e < valid ? ((const uint16_t*)p)[e] : 0u;
-            const unsigned hi = e + 1 < valid ? ((const uint16_t*)p)[e + 1] : 0u;
+            const unsigned lo = e < valid ? (unsigned)ld_g<uint16_t>(p + 2 * e) : 0u;
+            const unsigned hi = e + 1 < valid ? (unsigned)ld_g<uint16_t>(p + 2 * (e + 1)) : 0u;
             x[e >> 1] = pack2(lo, hi);
         }
         return x;
@@ -390,13 +390,13 @@ struct VgOperand {
                 const int rr = idx / C::CPA, gk = k0 + (idx % C::CPA) * 8;
                 if (rr < Mrel && gk < kend) {
                     const char* p = Apanel + ((int64_t)rr * K + gk) * 2;
-                    x = gk + 8 <= kend ? *(const u32x4_u*)p : gather(p, kend - gk);
+                    x = gk + 8 <= kend ? ld_g<u32x4_u>(p) : gather(p, kend - gk);
                 }
             } else {
                 const int gk = k0 + idx / C::CPB, gn = n0 + (idx % C::CPB) * 8;
                 if (gk < kend && gn < N) {
                     const char* p = Bbatch + ((int64_t)gk * N + gn) * 2;
-                    x = gn + 8 <= N ? *(const u32x4_u*)p : gather(p, N - gn);
+                    x = gn + 8 <= N ? ld_g<u32x4_u>(p) : gather(p, N - gn);
                 }
             }
             r[v] = x;

@@ -37,6 +37,21 @@ typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 // unaligned mode, so these still compile to single 8/16-byte global accesses.
 typedef unsigned u32x4_u __attribute__((ext_vector_type(4), aligned(2)));
 typedef unsigned u32x2_u __attribute__((ext_vector_type(2), aligned(2)));
+// Global memory through address-space-1 pointers.  The operand and result
+// pointers arrive in a by-value argument struct, from which the compiler
+// cannot infer their address space: a plain dereference would compile to a
+// flat access, which also counts against the LDS wait counter, so every wait
+// for an LDS read would wait for the global loads in flight as well.
+template <class T>
+__device__ __forceinline__ T ld_g(const void* p)
+{
+    return *(const __attribute__((address_space(1))) T*)p;
+}
+template <class T>
+__device__ __forceinline__ void st_g(void* p, T v)
+{
+    *(__attribute__((address_space(1))) T*)p = v;
+}
 // LDS pointers stay in address space 3 from the __shared__ object onwards, so
 // every LDS access compiles to a ds_* instruction with no generic-address
 // detour.
@@ -129,12 +144,12 @@ struct Tile {
             const int gm = m0 + r, gk = k0 + c * C::VE;
             const char* p = Ab + ((int64_t)gm * K + gk) * C::EB;
             if (C::VEC) {
-                ra[v] = (gm < M && gk < kend) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
+                ra[v] = (gm < M && gk < kend) ? ld_g<u32x4>(p) : u32x4{0, 0, 0, 0};
             } else {
                 u32x4 x = {0, 0, 0, 0};
                 if (gm < M) {
                     if (gk + C::VE <= kend)
-                        x = *(const u32x4_u*)p;
+                        x = ld_g<u32x4_u>(p);
                     else
                         x = gather_row(p, kend - gk);
                 }
@@ -153,12 +168,12 @@ struct Tile {
                     const int gk = k0 + kb * C::BK + r;
                     const char* p = Bb + ((int64_t)gk * N + gn) * 2;
                     if (C::VEC) {
-                        rb[i * C::BK + r] = (gk < kend && gn < N) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
+                        rb[i * C::BK + r] = (gk < kend && gn < N) ? ld_g<u32x4>(p) : u32x4{0, 0, 0, 0};
                     } else {
                         u32x4 x = {0, 0, 0, 0};
                         if (gk < kend) {
                             if (gn + 8 <= N)
-                                x = *(const u32x4_u*)p;
+                                x = ld_g<u32x4_u>(p);
                             else
                                 x = gather_row(p, N - gn);
                         }
@@ -175,12 +190,12 @@ struct Tile {
                 const int gn = n0 + c * 4, gk = k0 + kr;
                 const char* p = Bb + ((int64_t)gk * N + gn) * 4;
                 if (C::VEC) {
-                    rb[v] = (gk < kend && gn < N) ? *(const u32x4*)p : u32x4{0, 0, 0, 0};
+                    rb[v] = (gk < kend && gn < N) ? ld_g<u32x4>(p) : u32x4{0, 0, 0, 0};
                 } else {
                     u32x4 x = {0, 0, 0, 0};
                     if (gk < kend) {
                         if (gn + 4 <= N)
-                            x = *(const u32x4_u*)p;
+                            x = ld_g<u32x4_u>(p);
                         else
                             x = gather_row(p, N - gn);
                     }
@@ -211,7 +226,7 @@ struct Tile {
             for (int v = 0; v < C::AV; ++v) {
                 u32x4 x = {0, 0, 0, 0};
                 if (kin && (unsigned)(ca.ih0[v] + dh) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dw) < (unsigned)p.cW)
-                    x = *(const u32x4_u*)(X + (ca.pix[v] + koff) * C::EB);
+                    x = ld_g<u32x4_u>(X + (ca.pix[v] + koff) * C::EB);
                 ra[v] = x;
             }
             return;
@@ -249,7 +264,7 @@ struct Tile {
             unsigned e16[C::VE];
             if (one_row && (unsigned)(ca.ih0[v] + dhe[0]) < (unsigned)p.cH && ca.iw0[v] + dwe[0] >= 0 &&
                 ca.iw0[v] + kw_last < p.cW) {
-                ra[v] = *(const u32x4_u*)(X + (ca.pix[v] + koff[0]) * C::EB);
+                ra[v] = ld_g<u32x4_u>(X + (ca.pix[v] + koff[0]) * C::EB);
                 continue;
             }
 #pragma unroll
@@ -257,7 +272,7 @@ struct Tile {
                 unsigned val = 0u;
                 if ((unsigned)(ca.ih0[v] + dhe[e]) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dwe[e]) < (unsigned)p.cW) {
                     const char* src = X + (ca.pix[v] + koff[e]) * C::EB;
-                    val = C::H ? (unsigned)*(const uint16_t*)src : *(const unsigned*)src;
+                    val = C::H ? (unsigned)ld_g<uint16_t>(src) : ld_g<unsigned>(src);
                 }
                 e16[e] = val;
             }
@@ -282,14 +297,14 @@ struct Tile {
         if (C::H) {
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const unsigned lo = e < valid ? ((const uint16_t*)p)[e] : 0u;
-                const unsigned hi = e + 1 < valid ? ((const uint16_t*)p)[e + 1] : 0u;
+                const unsigned lo = e < valid ? (unsigned)ld_g<uint16_t>(p + 2 * e) : 0u;
+                const unsigned hi = e + 1 < valid ? (unsigned)ld_g<uint16_t>(p + 2 * (e + 1)) : 0u;
                 x[e >> 1] = pack2(lo, hi);
             }
         } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                x[e] = e < valid ? ((const unsigned*)p)[e] : 0u;
+                x[e] = e < valid ? ld_g<unsigned>(p + 4 * e) : 0u;
         }
         return x;
     }
@@ -433,12 +448,12 @@ __device__ __forceinline__ void store4(char* __restrict__ Cb, int64_t off, int n
     if (DT == DT_F32) {
         float* p = (float*)Cb + off;
         if (n + 3 < N) {
-            *(u32x4_u*)p = __builtin_bit_cast(u32x4, f32x4{a0, a1, a2, a3});
+            st_g<u32x4_u>(p, __builtin_bit_cast(u32x4, f32x4{a0, a1, a2, a3}));
         } else {
-            if (n < N) p[0] = a0;
-            if (n + 1 < N) p[1] = a1;
-            if (n + 2 < N) p[2] = a2;
-            if (n + 3 < N) p[3] = a3;
+            if (n < N) st_g<float>(p, a0);
+            if (n + 1 < N) st_g<float>(p + 1, a1);
+            if (n + 2 < N) st_g<float>(p + 2, a2);
+            if (n + 3 < N) st_g<float>(p + 3, a3);
         }
     } else {
         uint16_t h[4];
@@ -455,12 +470,12 @@ __device__ __forceinline__ void store4(char* __restrict__ Cb, int64_t off, int n
         }
         uint16_t* p = (uint16_t*)Cb + off;
         if (n + 3 < N) {
-            *(u32x2_u*)p = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+            st_g<u32x2_u>(p, u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])});
         } else {
-            if (n < N) p[0] = h[0];
-            if (n + 1 < N) p[1] = h[1];
-            if (n + 2 < N) p[2] = h[2];
-            if (n + 3 < N) p[3] = h[3];
+            if (n < N) st_g<uint16_t>(p, h[0]);
+            if (n + 1 < N) st_g<uint16_t>(p + 1, h[1]);
+            if (n + 2 < N) st_g<uint16_t>(p + 2, h[2]);
+            if (n + 3 < N) st_g<uint16_t>(p + 3, h[3]);
         }
     }
 }
@@ -799,15 +814,15 @@ __device__ __forceinline__ void store_lds(const VxGemmArgs& p, Acc<C>& acc, cons
         const u32x4 v = *(lds_u32x4*)(buf + (r * LDC + c * VE) * EB);
         char* dst = Cb + ((int64_t)m * p.N + n) * EB;
         if (n + VE <= p.N) {
-            *(u32x4_u*)dst = v;
+            st_g<u32x4_u>(dst, v);
         } else {
 #pragma unroll
             for (int e = 0; e < VE; ++e)
                 if (n + e < p.N) {
                     if constexpr (EB == 2)
-                        ((uint16_t*)dst)[e] = (uint16_t)elem16(v, e);
+                        st_g<uint16_t>(dst + 2 * e, (uint16_t)elem16(v, e));
                     else
-                        ((unsigned*)dst)[e] = v[e];
+                        st_g<unsigned>(dst + 4 * e, v[e]);
                 }
         }
     }

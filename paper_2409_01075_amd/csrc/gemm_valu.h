@@ -112,7 +112,7 @@ __device__ __forceinline__ void gemm_valu_body(const VxGemmArgs& args)
             const int m = q / cpr, kc = q % cpr;
             u32x4 v = {0, 0, 0, 0};
             if (m < Mrel && kc * C::VE < kv)
-                v = *(const u32x4*)(Ab + ((int64_t)m * p.K + kc * C::VE) * C::EB);
+                v = ld_g<u32x4>(Ab + ((int64_t)m * p.K + kc * C::VE) * C::EB);
 #pragma unroll
             for (int w = 0; w < 4; ++w)              // 4 words of PK elements per chunk
                 *(__attribute__((address_space(3))) unsigned*)(lds + ((kc * 4 + w) * C::MT + m) * 4) = v[w];
