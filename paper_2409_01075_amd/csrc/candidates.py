@@ -372,6 +372,35 @@ def mixed_candidates(base, hw=GFX950):
     return out
 
 
+# Short-K tiles (fp16/bf16, direct-to-LDS, 2-stage rings of Kb = 32): a GEMM
+# whose K is one or two steps of the usual Kb = 64 (the attention scores
+# Q x K^T, K = head size 64) has nothing to overlap with its only K step's
+# loads.  With Kb = 32 the second step's DMA flies while the first computes,
+# and the ring alone (2 x (Mb + Nb) x 32 x 2 bytes) is smaller than the C tile
+# staged for the LDS epilogue, so the LDS is sized for the staged tile
+# instead.  Three tiles, each with both operands by DMA and with B through
+# VGPRs (rows not 16-byte aligned, odd lengths).
+SHORT_K_TILES = ((128, 128, 32, 2, 2, 32), (128, 128, 32, 4, 2, 16), (128, 256, 32, 2, 4, 32))
+
+
+def short_k_candidates(dtype, hw=GFX950):
+    out = []
+    for (mb, nb, kb, wm, wn, mi) in SHORT_K_TILES:
+        nt = wm * wn * hw["wave"]
+        lds = max(lds_bytes_dma(mb, nb, kb, 2), mb * (nb + 8) * 2)
+        for vg in (0, 2):
+            if vg == 2 and (kb * (nb // 8)) % nt:
+                continue
+            e = _entry(dtype, "dma", 2, (mb, nb, kb, wm, wn, mi), 1 if vg == 0 else 0, hw)
+            e["lds"] = lds
+            e["fit_c"] = 1
+            if vg:
+                e["vg"] = vg
+                e["align"] = 1
+            out.append(e)
+    return out
+
+
 def registry(hw=GFX950):
     """All workgroup-level candidates that are compiled into the library.
 
@@ -405,6 +434,8 @@ def registry(hw=GFX950):
         out += dma_wide_candidates(dtype, hw)
     out += pingpong_candidates(list(out))
     out += mixed_candidates(list(out), hw)
+    for dtype in ("f16", "bf16"):
+        out += short_k_candidates(dtype, hw)
     for i, e in enumerate(out):
         e["id"] = i
     return out

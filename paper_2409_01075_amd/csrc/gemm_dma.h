@@ -43,7 +43,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, int ST_, bool VEC_, bool CONV_ = false,
-          bool PP_ = false, int VG_ = 0>
+          bool PP_ = false, int VG_ = 0, bool FITC_ = false>
 struct DCfg {
     static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_, STAGES = ST_;
     static constexpr bool VEC = VEC_;
@@ -55,6 +55,9 @@ struct DCfg {
     // aligned): 0 none, 1 A, 2 B
     static constexpr int VG = VG_;
     static constexpr bool DMA_A = VG != 1, DMA_B = VG != 2;
+    // LDS sized for the staged C tile as well as for the ring (short-K tiles
+    // whose ring alone is smaller than their C tile keep the LDS epilogue)
+    static constexpr bool FIT_C = FITC_;
     static constexpr bool H = true;
     static constexpr int EB = 2;
     static constexpr int NWAVE = WM * WN, NT = NWAVE * 64;
@@ -65,7 +68,10 @@ struct DCfg {
     static constexpr int A_BYTES = MB * KB * 2, B_BYTES = KB * NB * 2;
     static constexpr int CPA_ = KB / 8, CPB_ = NB / 8;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-    static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;   // the whole ring
+    static constexpr int RING_BYTES = STAGES * STAGE_BYTES;
+    static constexpr int LDC = NB + 8;
+    // the whole ring (with FIT_C, at least the staged C tile, MB x LDC)
+    static constexpr int LDS_BYTES = FIT_C && MB * LDC * 2 > RING_BYTES ? MB * LDC * 2 : RING_BYTES;
     static constexpr int CPA = KB / 8, CPB = NB / 8;       // 16-byte chunks per row
     static constexpr int SWA = CPA < 16 ? CPA : 16;        // A swizzle period (rows)
     static constexpr int LANE_BYTES = 16;                  // bytes one lane moves per DMA instruction
@@ -81,7 +87,6 @@ struct DCfg {
     // it issued whole right after the barrier, a full step before its use.
     static constexpr bool SPREAD_DMA = STAGES >= 3;
     // epilogue through LDS (store_lds) when the C tile fits the idle ring
-    static constexpr int LDC = NB + 8;
     static constexpr bool LDS_EPI = MB * LDC * 2 <= LDS_BYTES;
 
     static_assert(VEC, "direct-to-LDS loads move 16-byte chunks");
