@@ -13,9 +13,13 @@ device's CU count - never from application shapes:
 
 Each pair gives the time of one workgroup K step (difference over the extra steps) and
 the fixed per-call cost (the remainder, less the launch floor).  With the
-device full, the kernel also runs split-K with 2 and 4 slices of 2 steps each:
-the extra time over the unsplit 2-step call gives the split-K epilogue cost
-a + b * (slices - 1) (partial tile out, arrival counter, last slice's reads).
+device full, the kernel also runs split-K with 2, 3, 4, 6 and 8 slices of 2 steps
+each: the extra time over the unsplit 2-step call, fitted by least squares, gives the
+split-K epilogue cost a + b * (slices - 1) (partial tile out, arrival counter, last
+slice's reads).  A convolution kernel that gathers the image through VGPRs
+is also timed (2 and 10 steps, full and light load) on a convolution whose every image
+chunk must be gathered element by element (one channel, a filter dilated
+along the width): the selector adds the share of such chunks a layer has.
 A spin kernel ahead of each timed window lets the host queue every call before
 the device starts, so the times are device times, not host enqueue times.  Operands are
 cycled through device copies totalling at least 256 MiB, so steady-state
@@ -48,6 +52,23 @@ def _timer(stream, cycles_per_ms):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e6 / n      # ns per call
     return run
+
+
+# K slices at which the split-K epilogue is timed; its cost over the unsplit
+# call is fitted as a + b * (slices - 1) by least squares (a difference of
+# two timings alone moved b by a factor of 3 between runs).
+SPLITS = (2, 3, 4, 6, 8)
+
+
+def _split_fit(pts):
+    """Least-squares line through (slices - 1, extra ns) points; a, b >= 0."""
+    n = float(len(pts))
+    mx = sum(x for x, _ in pts) / n
+    my = sum(y for _, y in pts) / n
+    sxx = sum((x - mx) ** 2 for x, _ in pts)
+    b = max(sum((x - mx) * (y - my) for x, y in pts) / sxx, 0.0) if sxx > 0 else 0.0
+    a = max(my - b * mx, 0.0)
+    return a, b
 
 
 def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
@@ -89,7 +110,7 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
         meas = {}
         eb = 4 if k.dtype == 0 else 2
 
-        def timed(M, N, K, split):
+        def timed(M, N, K, split, gather=False):
             set_bytes = (M * K + K * N + M * N) * eb
             R = int(min(max(2, -(-rot_mib * 2 ** 20 // set_bytes)), 512))
             # an operand whose rows the kernel does not need aligned is timed
@@ -105,8 +126,17 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
             sa, sb, sc = M * K * eb, K * N * eb, M * N * eb
             vx.vx_force_plan(kid, split)
             # a convolution kernel runs the same implicit-GEMM shape as a 1 x 1
-            # convolution of a 1 x M image with K channels into N
-            desc = vx.conv_desc(1, 1, M, K, N, 1, 1, k.dtype) if k.op == 1 else None
+            # convolution of a 1 x M image with K channels into N; with `gather`,
+            # as an M x 1 output of one channel under a (K / VE) x VE filter
+            # dilated 2 along the width, so that every chunk of VE consecutive k
+            # is gathered element by element
+            desc = None
+            if k.op == 1 and gather:
+                ve = 16 // eb
+                kh = K // ve
+                desc = vx.conv_desc(1, M + kh - 1, 1 + 2 * (ve - 1), 1, N, kh, ve, k.dtype, dil=(1, 2))
+            elif k.op == 1:
+                desc = vx.conv_desc(1, 1, M, K, N, 1, 1, k.dtype)
             try:
                 def call(i):
                     r = i % R
@@ -119,7 +149,7 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
                 call(0)
                 torch.cuda.synchronize()
                 calls = max(R, 16)
-                return float(np.median([run(call, calls) for _ in range(3)]))
+                return float(np.median([run(call, calls) for _ in range(5)]))
             finally:
                 vx.vx_force_plan(-1, 0)
 
@@ -131,21 +161,32 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
             mt = G // nt
             for nk in (2, nk_hi):
                 meas[(tag, nk)] = timed(mt * k.mb, nt * k.nb, nk * k.kb, 1)
-        for s_ in (2, 4):
+        for s_ in SPLITS:
             tiles = max(1, slots // s_)
             nt = min(16, tiles)
             mt = max(1, tiles // nt)
             meas[("split", s_)] = timed(mt * k.mb, nt * k.nb, s_ * 2 * k.kb, s_)
+        # convolution kernels that gather the image through VGPRs: the K step
+        # when every image chunk is gathered element by element
+        gathers = k.op == 1 and not k.align & 1
+        if gathers:
+            for tag, G in (("gather", slots), ("gather_light", min(32, slots))):
+                nt = min(16, G)
+                mt = G // nt
+                for nk in (2, nk_hi):
+                    meas[(tag, nk)] = timed(mt * k.mb, nt * k.nb, nk * k.kb, 1, gather=True)
         step_full = max((meas[("full", nk_hi)] - meas[("full", 2)]) / (nk_hi - 2.0), 1.0)
+        step_gather = (max((meas[("gather", nk_hi)] - meas[("gather", 2)]) / (nk_hi - 2.0), 1.0) if gathers
+                       else -1.0)
+        step_gather_light = (max((meas[("gather_light", nk_hi)] - meas[("gather_light", 2)]) / (nk_hi - 2.0), 1.0)
+                             if gathers else -1.0)
         step_light = max((meas[("light", nk_hi)] - meas[("light", 2)]) / (nk_hi - 2.0), 1.0)
         fix_full = max(meas[("full", 2)] - 2 * step_full - launch, 0.0)
         fix_light = max(meas[("light", 2)] - 2 * step_light - launch, 0.0)
         load_light = min(32, slots) / float(slots)
-        o2 = max(meas[("split", 2)] - meas[("full", 2)], 0.0)
-        o4 = max(meas[("split", 4)] - meas[("full", 2)], 0.0)
-        split_b = max((o4 - o2) / 2.0, 0.0)
-        split_a = max(o2 - split_b, 0.0)
-        rows.append((kid, step_full, fix_full, step_light, fix_light, load_light, split_a, split_b))
+        split_a, split_b = _split_fit([(s_ - 1, max(meas[("split", s_)] - meas[("full", 2)], 0.0)) for s_ in SPLITS])
+        rows.append((kid, step_full, fix_full, step_light, fix_light, load_light, split_a, split_b, step_gather,
+                     step_gather_light))
         if verbose:
             print("kernel %3d %-28s occ %d  step %8.1f / %8.1f ns  fixed %8.1f / %8.1f ns  split %7.1f + %7.1f"
                   " (%.0f s)" % (kid, "%dx%dx%d w%dx%d st%d f%d v%d" % (k.mb, k.nb, k.kb, k.wm, k.wn, k.stages,
@@ -156,13 +197,13 @@ def calibrate(out=None, dtypes=(0, 1, 2), rot_mib=256, verbose=True):
     with open(out, "w") as f:
         f.write("# vx kernel calibration (offline, per device): written by paper_2409_01075_amd/calibrate.py\n")
         f.write("# kernel <id> <step_full_ns> <fixed_full_ns> <step_light_ns> <fixed_light_ns> <load_light>"
-                " <split_a_ns> <split_b_ns>\n")
+                " <split_a_ns> <split_b_ns> <step_gather_full_ns> <step_gather_light_ns>\n")
         f.write("arch %s\n" % arch)
         f.write("device_cus %d\n" % hw.num_cu)
         f.write("registry_hash %s\n" % vx.vx_registry_hash())
         f.write("launch_ns %.1f\n" % launch)
         for r in rows:
-            f.write("kernel %d %.1f %.1f %.1f %.1f %.5f %.1f %.1f\n" % r)
+            f.write("kernel %d %.1f %.1f %.1f %.1f %.5f %.1f %.1f %.1f %.1f\n" % r)
     if verbose:
         print("wrote %s (%d kernels, launch floor %.0f ns)" % (out, len(rows), launch), file=sys.stderr)
     return out

@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <string>
 #include <vector>
@@ -49,11 +50,12 @@ struct PlanKey {
     int64_t tickets;
     uint64_t epoch;
     int op;
+    int gather_pm;   // convolution: the share of image chunks gathered element by element, per mille
     bool operator==(const PlanKey& o) const
     {
         return batch == o.batch && M == o.M && N == o.N && K == o.K && dt == o.dt && vec_ok == o.vec_ok &&
                c_vec == o.c_vec && dev == o.dev && ws == o.ws && tickets == o.tickets && epoch == o.epoch &&
-               op == o.op;
+               op == o.op && gather_pm == o.gather_pm;
     }
 };
 uint64_t plan_hash(const PlanKey& k)
@@ -62,7 +64,7 @@ uint64_t plan_hash(const PlanKey& k)
     auto mix = [&h](uint64_t v) { h = (h ^ v) * 1099511628211ull; };
     mix(k.batch); mix(k.M); mix(k.N); mix(k.K);
     mix(k.dt | (k.vec_ok << 4) | (k.c_vec << 5) | (k.op << 6) | ((uint64_t)k.dev << 8));
-    mix(k.ws); mix(k.tickets); mix(k.epoch);
+    mix(k.ws); mix(k.tickets); mix(k.epoch); mix((uint64_t)k.gather_pm);
     return h ^ (h >> 29);
 }
 
@@ -184,9 +186,10 @@ int load_calib_file(const char* path, const char* arch)
         else if (!strcmp(key, "kernel")) {
             int id;
             VxCalib c;
-            c.split_a = c.split_b = -1.0;
-            if (sscanf(line, "%*s %d %lf %lf %lf %lf %lf %lf %lf", &id, &c.step_full, &c.fix_full, &c.step_light,
-                       &c.fix_light, &c.load_light, &c.split_a, &c.split_b) >= 6 &&
+            c.split_a = c.split_b = c.step_gather = c.step_gather_light = -1.0;
+            if (sscanf(line, "%*s %d %lf %lf %lf %lf %lf %lf %lf %lf %lf", &id, &c.step_full, &c.fix_full,
+                       &c.step_light, &c.fix_light, &c.load_light, &c.split_a, &c.split_b, &c.step_gather,
+                       &c.step_gather_light) >= 6 &&
                 id >= 0 && id < n && c.step_full > 0.0 && c.step_light > 0.0 && c.load_light > 0.0) {
                 cal[id] = c;
                 ok[id] = 1;
@@ -276,7 +279,8 @@ vx_status plan_for(int dev, const VxShape& sh, size_t ws_bytes, int64_t tickets,
     // under a stale epoch and never found again
     const uint64_t epoch = g_epoch.load();
     const int forced = g_force_id.load();
-    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, tickets, epoch, sh.op};
+    PlanKey key{sh.batch, sh.M, sh.N, sh.K, sh.dt, sh.vec_ok, sh.c_vec, dev, ws_bytes, tickets, epoch, sh.op,
+                (int)(sh.gather_frac * 1000.0 + 0.5)};
     if (forced < 0 && cache_find(key, out))
         return VX_OK;
     VxFilter f;
@@ -611,7 +615,21 @@ vx_status conv_shape(const vx_conv2d_desc* d, VxShape* sh, VxGemmArgs* a, bool* 
     // image offsets are 32-bit (operand alignment is checked by the caller
     // that has the pointers); vec_ok is part of the plan cache's key
     sh->a_bytes = (int64_t)((double)d->n * d->h * d->w * d->c_in) * elem_bytes(d->dtype);
-    sh->vec_ok = d->dtype != VX_F32 && d->c_in % 8 == 0 && d->c_out % 8 == 0 && sh->a_bytes < ((int64_t)1 << 31) ? 3 : 0;
+    // bit 0: the image (16-byte chunks of 8 channels, 32-bit image offsets);
+    // bit 1: the filter (rows of c_out elements)
+    sh->vec_ok = (d->dtype != VX_F32 && d->c_in % 8 == 0 && sh->a_bytes < ((int64_t)1 << 31) ? 1 : 0) |
+                 (d->dtype != VX_F32 && d->c_out % 8 == 0 ? 2 : 0);
+    // the kernels that gather the image through VGPRs load a 16-byte chunk
+    // (ve consecutive k) as one vector when the channels come in whole chunks,
+    // or when, with unit width dilation, the chunk stays inside the kw * c_in
+    // contiguous elements of one filter row; otherwise element by element.
+    // Chunk starts fall evenly over a filter row, so (ve - 1) of every kw * c_in
+    // positions cross its end (taps in the padding aside)
+    {
+        const int ve = 16 / elem_bytes(d->dtype);
+        const double run = (double)d->kw * (double)d->c_in;
+        sh->gather_frac = d->c_in % ve == 0 ? 0.0 : (d->dil_w != 1 || run < ve) ? 1.0 : std::min(1.0, (ve - 1) / run);
+    }
     sh->c_vec = 0;
     sh->op = 1;
     a->cH = (int)d->h;
@@ -776,7 +794,7 @@ vx_status vx_conv2d(const vx_conv2d_desc* d, const void* x, const void* w, void*
         return VX_ERR_INVALID_ARG;
     if (empty)
         return VX_OK;
-    sh.vec_ok = sh.vec_ok && (uintptr_t)x % 16 == 0 && (uintptr_t)w % 16 == 0 ? 3 : 0;
+    sh.vec_ok &= ((uintptr_t)x % 16 == 0 ? 1 : 0) | ((uintptr_t)w % 16 == 0 ? 2 : 0);
     a.A = x;
     a.B = w;
     a.C = y;

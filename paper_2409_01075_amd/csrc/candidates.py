@@ -287,6 +287,29 @@ def conv_dma_candidates(dtype, hw=GFX950):
     return out
 
 
+# fp16/bf16 convolutions whose channel count is not a multiple of 8 (the
+# image's 16-byte chunks do not start on tap boundaries) but whose filter rows
+# are (c_out a multiple of 8): the filter by DMA and the image through VGPRs
+# with the register-staged kernels' im2col gather, into the same LDS layout
+# (mixed loads, VG 1).  The 2-stage direct-to-LDS convolution tiles of at
+# least 64 x 128 whose image chunks split evenly over the threads (a 64 x 64
+# mixed tile ran small layers up to 1.5x slower than the register-staged
+# tiles the selector would otherwise take, and won only some by up to 1.5x).
+def conv_mixed_candidates(dtype, hw=GFX950):
+    out = []
+    for e in conv_dma_candidates(dtype, hw):
+        nt = e["wm"] * e["wn"] * hw["wave"]
+        chunks = e["mb"] * (e["kb"] // 8)
+        if e["stages"] != 2 or chunks % nt or chunks // nt > 16 or e["mb"] * e["nb"] < 64 * 128:
+            continue
+        m = dict(e)
+        m["vg"] = 1
+        m["vec"] = 0
+        m["align"] = 2
+        out.append(m)
+    return out
+
+
 # ------------------------------------------------- vector-ALU family (L0') --
 # The adaptive second backend for small M (the paper's CUDA-core path next to
 # the tensor-core path): level 0 is one lane's MT x VE outputs computed with
@@ -436,6 +459,8 @@ def registry(hw=GFX950):
     out += mixed_candidates(list(out), hw)
     for dtype in ("f16", "bf16"):
         out += short_k_candidates(dtype, hw)
+    for dtype in ("f16", "bf16"):
+        out += conv_mixed_candidates(dtype, hw)
     for i, e in enumerate(out):
         e["id"] = i
     return out

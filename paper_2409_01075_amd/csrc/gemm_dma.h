@@ -94,8 +94,10 @@ struct DCfg {
     static_assert(KB % KI == 0 && KB % 8 == 0 && NB % 8 == 0, "K step and chunking");
     static_assert(!DMA_A || (A_IPW >= 1 && A_IPW * WAVE_BYTES * NWAVE == A_BYTES), "A DMA must split evenly over waves");
     static_assert(!DMA_B || (B_IPW >= 1 && B_IPW * WAVE_BYTES * NWAVE == B_BYTES), "B DMA must split evenly over waves");
-    static_assert(VG == 0 || (STAGES == 2 && !CONV && !PP && VGC >= 1 && VGC * NT == (VG == 1 ? MB * CPA : KB * CPB)),
-                  "an operand through VGPRs: 2-stage ring, chunks split evenly over the threads");
+    static_assert(VG == 0 || (STAGES == 2 && (!CONV || VG == 1) && !PP && VGC >= 1 &&
+                              VGC * NT == (VG == 1 ? MB * CPA : KB * CPB)),
+                  "an operand through VGPRs: 2-stage ring, chunks split evenly over the threads (a convolution's "
+                  "image only)");
     static_assert(STAGES >= 2 && STAGES <= 16, "pipeline depth");
     static_assert((STAGES - 1) * LPS <= 63, "vmcnt range: the prologue's DMA all in flight");
     static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
@@ -234,8 +236,9 @@ __device__ __forceinline__ void dma_lds(const u32x4& r, lds_char* dst, unsigned 
 // host keeps H + 2 pad and W + 2 pad below 2^30).
 template <class C>
 struct DmaConvA {
-    unsigned pix[C::A_IPW];   // element offset of (n, ih0, iw0), mod 2^32
-    int ih0[C::A_IPW], iw0[C::A_IPW];
+    static constexpr int NA = C::A_IPW > 0 ? C::A_IPW : 1;
+    unsigned pix[NA];   // element offset of (n, ih0, iw0), mod 2^32
+    int ih0[NA], iw0[NA];
     int gk, ci, kw, kh;
 
     __device__ __forceinline__ void init(const VxGemmArgs& p, int m0, int kbeg, int wave, int lane)
@@ -408,6 +411,16 @@ struct VgOperand {
         }
     }
 
+    // A convolution's A (VG 1): the K step at the chunk column held in the
+    // im2col map state `ca`, gathered as the register-staged kernels do; a
+    // thread's VGC chunks are rows (t + v NT) / CPA at chunk column t % CPA.
+    template <class CA>
+    __device__ __forceinline__ void load_conv(const VxGemmArgs& p, const char* X, const CA& ca, int kend)
+    {
+        static_assert(C::VG == 1 && C::CONV, "the image through VGPRs");
+        conv_gather<CA, C::VGC, 8, true, 2>(p, X, ca, kend, r);
+    }
+
     __device__ __forceinline__ void store(lds_char* stage, int t) const
     {
 #pragma unroll
@@ -424,6 +437,15 @@ struct VgOperand {
             *(lds_u32x4*)dst = r[v];
         }
     }
+};
+
+// The im2col map state of the register-staged kernels (ConvA) over the rows
+// and the chunk column that the VGPR loads of a mixed convolution tile take.
+template <class D>
+struct VgConvView {
+    static constexpr int KB = D::KB, VE = 8, NT = D::NT, AV = D::VGC;
+    static constexpr bool CONV = true;
+    static_assert(D::CPA == KB / VE, "a row of the K step is CPA chunks");
 };
 
 // Level 0 over one LDS stage.  The fragments of MFMA step kk+1 are read from
@@ -551,7 +573,7 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
     // last STAGES-2 iterations (the drain) the count falls to 0.
     // prologue: the first min(STAGES-1, nk) K steps, step s into stage s
     DmaConvA<C> cv;
-    if constexpr (C::CONV)
+    if constexpr (C::CONV && C::VG == 0)
         cv.init(p, g.m0, g.kbeg, wave, lane);
     // the DMA of the K step at k0 into stage st (for a convolution, at the
     // map state's step, which then moves on: steps are made in order)
@@ -590,9 +612,22 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
         // The VGPR loads of step it+1 fly with its DMA while step it computes,
         // then land in the free stage before the next barrier.
         VgOperand<C> vg;
+        // a convolution's image goes through the im2col map, whose state
+        // advances one K step per load (the steps come in order)
+        ConvA<VgConvView<C>> ca;
+        if constexpr (C::CONV)
+            ca.init(p, g.m0, g.kbeg, t);
+        auto vg_load = [&](int k0) {
+            if constexpr (C::CONV) {
+                vg.load_conv(p, (const char*)p.A, ca, g.kend);
+                ca.advance(p);
+            } else {
+                vg.load(Apanel, Bbatch, k0, g.kend, Mrel, g.n0, p.N, p.K, t);
+            }
+        };
         const DmaTile<C> none(VX_STAGE(0), Apanel, Bbatch, g.kbeg, g.kend, g.n0, p.N);
         if (g.nk > 0) {
-            vg.load(Apanel, Bbatch, g.kbeg, g.kend, Mrel, g.n0, p.N, p.K, t);
+            vg_load(g.kbeg);
             wait_vm<0>();
             vg.store(VX_STAGE(0), t);
         }
@@ -608,7 +643,7 @@ __device__ __forceinline__ void gemm_dma_body(const VxGemmArgs& args)
                 if (more) {
                     const int k1 = g.kbeg + (it + 1) * C::KB;
                     DmaTile<C>(VX_STAGE(j ^ 1), Apanel, Bbatch, k1, g.kend, g.n0, p.N).issue(Mrel, p.N, p.K, wave, lane);
-                    vg.load(Apanel, Bbatch, k1, g.kend, Mrel, g.n0, p.N, p.K, t);
+                    vg_load(k1);
                 }
                 __builtin_amdgcn_sched_barrier(0);
                 dma_compute<C>(VX_STAGE(j), acc, wm0, wn0, lane, none, false, Mrel, p.N, p.K, wave);

@@ -119,6 +119,90 @@ __device__ __forceinline__ unsigned elem16(const u32x4& v, int j)
     return (j & 1) ? hi16(w) : lo16(w);
 }
 
+// A of a convolution for one K step: the chunk column held in `ca` (see
+// ConvA) of AV rows, gathered from the image X through the im2col map.  Row gm
+// of the implicit A is output pixel (n, oh, ow); column gk is filter tap
+// (kh, kw) and input channel ci, with gk = (kh * KW + kw) * Cin + ci.  When
+// Cin is a multiple of the chunk, a chunk never straddles two taps and is one
+// 16-byte load (or zeros in the padding); otherwise it is gathered element by
+// element, except where it stays inside one filter row (see below).  Taps in
+// the padding and k at or past kend read as zeros.
+template <class CA, int AV, int VE, bool H, int EB>
+__device__ __forceinline__ void conv_gather(const VxGemmArgs& p, const char* __restrict__ X, const CA& ca, int kend,
+                                            u32x4 (&ra)[AV])
+{
+    if (p.cC % VE == 0) {   // wave-uniform: a chunk is VE channels of one tap
+        const int dh = ca.kh * p.cdh, dw = ca.kw * p.cdw;
+        const int64_t koff = ((int64_t)dh * p.cW + dw) * p.cC + ca.ci;
+        const bool kin = ca.gk < kend;
+#pragma unroll
+        for (int v = 0; v < AV; ++v) {
+            u32x4 x = {0, 0, 0, 0};
+            if (kin && (unsigned)(ca.ih0[v] + dh) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dw) < (unsigned)p.cW)
+                x = ld_g<u32x4_u>(X + (ca.pix[v] + koff) * EB);
+            ra[v] = x;
+        }
+        return;
+    }
+    // channels not a multiple of the chunk: the VE elements of a chunk walk
+    // over channels, then filter columns, then filter rows
+    int ci = ca.ci, kw = ca.kw, kh = ca.kh;
+    int dhe[VE], dwe[VE];
+    int64_t koff[VE];
+#pragma unroll
+    for (int e = 0; e < VE; ++e) {
+        dhe[e] = ca.gk + e < kend ? kh * p.cdh : -(1 << 30);   // k past kend: an out-of-range row
+        dwe[e] = kw * p.cdw;
+        koff[e] = ((int64_t)(kh * p.cdh) * p.cW + dwe[e]) * p.cC + ci;
+        if (++ci == p.cC) {
+            ci = 0;
+            if (++kw == p.cKW) {
+                kw = 0;
+                ++kh;
+            }
+        }
+    }
+    // With unit dilation along the width, the KW x Cin elements of one filter
+    // row are contiguous in the NHWC image (k = kw Cin + ci maps to kw Cin + ci
+    // elements past the row's first tap): a chunk that stays within one filter
+    // row, below kend, whose first and last taps fall inside the image, is one
+    // 16-byte (unaligned) load.  The chunk's first tap is at column ca.kw, its
+    // last at kw_last (same row ca.kh).
+    const int run = p.cKW * p.cC;                  // elements of one filter row
+    const int j0 = ca.kw * p.cC + ca.ci;           // the chunk's first element within its row
+    const bool one_row = p.cdw == 1 && j0 + VE <= run && ca.gk + VE <= kend;
+    const int kw_last = (j0 + VE - 1) / p.cC;
+#pragma unroll
+    for (int v = 0; v < AV; ++v) {
+        unsigned e16[VE];
+        if (one_row && (unsigned)(ca.ih0[v] + dhe[0]) < (unsigned)p.cH && ca.iw0[v] + dwe[0] >= 0 &&
+            ca.iw0[v] + kw_last < p.cW) {
+            ra[v] = ld_g<u32x4_u>(X + (ca.pix[v] + koff[0]) * EB);
+            continue;
+        }
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+            unsigned val = 0u;
+            if ((unsigned)(ca.ih0[v] + dhe[e]) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dwe[e]) < (unsigned)p.cW) {
+                const char* src = X + (ca.pix[v] + koff[e]) * EB;
+                val = H ? (unsigned)ld_g<uint16_t>(src) : ld_g<unsigned>(src);
+            }
+            e16[e] = val;
+        }
+        u32x4 x;
+        if (H) {
+#pragma unroll
+            for (int e = 0; e < 8; e += 2)
+                x[e >> 1] = pack2(e16[e], e16[e + 1]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                x[e] = e16[e];
+        }
+        ra[v] = x;
+    }
+}
+
 template <class C>
 struct Tile {
     // ---------------------------------------------------------- Load (level 1)
@@ -205,89 +289,13 @@ struct Tile {
         }
     }
 
-    // Convolution: the A tile's chunks gathered from the image through the
-    // im2col map.  Row gm of the implicit A is output pixel (n, oh, ow);
-    // column gk is filter tap (kh, kw) and input channel ci, with
-    // gk = (kh * KW + kw) * Cin + ci.  When Cin is a multiple of the chunk,
-    // a chunk never straddles two taps and is one 16-byte load (or zeros in
-    // the padding); otherwise it is gathered element by element.
-    // A of a convolution: the K step at the chunk column held in `ca` (see
-    // ConvA), gathered through the im2col map; taps in the padding and k at or
-    // past kend read as zeros.
+    // A of a convolution: the K step at the chunk column held in `ca`,
+    // gathered through the im2col map (conv_gather).
     template <class CA>
     __device__ __forceinline__ void load_a_conv(const VxGemmArgs& p, const char* __restrict__ X, const CA& ca,
                                                 int kend)
     {
-        if (p.cC % C::VE == 0) {   // wave-uniform: a chunk is VE channels of one tap
-            const int dh = ca.kh * p.cdh, dw = ca.kw * p.cdw;
-            const int64_t koff = ((int64_t)dh * p.cW + dw) * p.cC + ca.ci;
-            const bool kin = ca.gk < kend;
-#pragma unroll
-            for (int v = 0; v < C::AV; ++v) {
-                u32x4 x = {0, 0, 0, 0};
-                if (kin && (unsigned)(ca.ih0[v] + dh) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dw) < (unsigned)p.cW)
-                    x = ld_g<u32x4_u>(X + (ca.pix[v] + koff) * C::EB);
-                ra[v] = x;
-            }
-            return;
-        }
-        // channels not a multiple of the chunk: the VE elements of a chunk walk
-        // over channels, then filter columns, then filter rows
-        int ci = ca.ci, kw = ca.kw, kh = ca.kh;
-        int dhe[C::VE], dwe[C::VE];
-        int64_t koff[C::VE];
-#pragma unroll
-        for (int e = 0; e < C::VE; ++e) {
-            dhe[e] = ca.gk + e < kend ? kh * p.cdh : -(1 << 30);   // k past kend: an out-of-range row
-            dwe[e] = kw * p.cdw;
-            koff[e] = ((int64_t)(kh * p.cdh) * p.cW + dwe[e]) * p.cC + ci;
-            if (++ci == p.cC) {
-                ci = 0;
-                if (++kw == p.cKW) {
-                    kw = 0;
-                    ++kh;
-                }
-            }
-        }
-        // With unit dilation along the width, the KW x Cin elements of one filter
-        // row are contiguous in the NHWC image (k = kw Cin + ci maps to kw Cin + ci
-        // elements past the row's first tap): a chunk that stays within one filter
-        // row, below kend, whose first and last taps fall inside the image, is one
-        // 16-byte (unaligned) load.  The chunk's first tap is at column ca.kw, its
-        // last at kw_last (same row ca.kh).
-        const int run = p.cKW * p.cC;                  // elements of one filter row
-        const int j0 = ca.kw * p.cC + ca.ci;           // the chunk's first element within its row
-        const bool one_row = p.cdw == 1 && j0 + C::VE <= run && ca.gk + C::VE <= kend;
-        const int kw_last = (j0 + C::VE - 1) / p.cC;
-#pragma unroll
-        for (int v = 0; v < C::AV; ++v) {
-            unsigned e16[C::VE];
-            if (one_row && (unsigned)(ca.ih0[v] + dhe[0]) < (unsigned)p.cH && ca.iw0[v] + dwe[0] >= 0 &&
-                ca.iw0[v] + kw_last < p.cW) {
-                ra[v] = ld_g<u32x4_u>(X + (ca.pix[v] + koff[0]) * C::EB);
-                continue;
-            }
-#pragma unroll
-            for (int e = 0; e < C::VE; ++e) {
-                unsigned val = 0u;
-                if ((unsigned)(ca.ih0[v] + dhe[e]) < (unsigned)p.cH && (unsigned)(ca.iw0[v] + dwe[e]) < (unsigned)p.cW) {
-                    const char* src = X + (ca.pix[v] + koff[e]) * C::EB;
-                    val = C::H ? (unsigned)ld_g<uint16_t>(src) : ld_g<unsigned>(src);
-                }
-                e16[e] = val;
-            }
-            u32x4 x;
-            if (C::H) {
-#pragma unroll
-                for (int e = 0; e < 8; e += 2)
-                    x[e >> 1] = pack2(e16[e], e16[e + 1]);
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    x[e] = e16[e];
-            }
-            ra[v] = x;
-        }
+        conv_gather<CA, C::AV, C::VE, C::H, C::EB>(p, X, ca, kend, ra);
     }
 
     // The first `valid` (< one chunk) elements of a row chunk, zeros after.

@@ -95,7 +95,7 @@ inline bool kernel_fits(const VxShape& sh, const vx_kernel_info& k, bool hyb, in
         // direct-to-LDS kernels address each K step with 32-bit buffer offsets:
         // Mb rows of A (Mb*K elements) and Kb rows of B (Kb*N elements); a
         // convolution's A offsets run over the whole image
-        const double a_span = k.op == 1 ? (double)sh.a_bytes : (double)k.mb * sh.K * eb;
+        const double a_span = k.op == 1 ? ((k.align & 1) ? (double)sh.a_bytes : 0.0) : (double)k.mb * sh.K * eb;
         if (a_span >= 2147483648.0 || (double)k.kb * sh.N * eb >= 2147483648.0)
             return false;
     }
@@ -180,9 +180,19 @@ double plan_cost(const vx_hwinfo& hw, const VxShape& sh, const vx_kernel_info& k
                 return light;
             return light + (full - light) * (load_last - cb->load_light) / (1.0 - cb->load_light);
         };
-        const double wave_full = cb->fix_full + (double)nk * cb->step_full;
-        const double wave_last = at_load(cb->fix_full, cb->fix_light) + (double)nk * at_load(cb->step_full, cb->step_light);
-        const double wave_dp = cb->fix_full + (double)nk_whole * cb->step_full;
+        // a convolution kernel that gathers the image through VGPRs pays for the
+        // share of chunks it must gather element by element (measured with every
+        // chunk so); the calibrated step has whole-chunk loads only
+        double step_full = cb->step_full, step_light = cb->step_light;
+        if (sh.op == 1 && sh.gather_frac > 0.0 && !(k.align & 1)) {
+            if (cb->step_gather > cb->step_full)
+                step_full += sh.gather_frac * (cb->step_gather - cb->step_full);
+            if (cb->step_gather_light > cb->step_light)
+                step_light += sh.gather_frac * (cb->step_gather_light - cb->step_light);
+        }
+        const double wave_full = cb->fix_full + (double)nk * step_full;
+        const double wave_last = at_load(cb->fix_full, cb->fix_light) + (double)nk * at_load(step_full, step_light);
+        const double wave_dp = cb->fix_full + (double)nk_whole * step_full;
         const double cost2 = (double)F_dp * wave_dp + (double)(F - 1) * wave_full + wave_last + t_split;
         return launch_cal + std::max(cost2, floor_ns);
     }

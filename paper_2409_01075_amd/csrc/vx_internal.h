@@ -23,6 +23,10 @@ const char* vxi_registry_hash(void);
 struct VxCalib {
     double step_full, fix_full, step_light, fix_light, load_light;
     double split_a, split_b;   // split-K epilogue: split_a + split_b * (slices - 1); < 0 if not measured
+    // convolution kernels that gather the image through VGPRs: one K step at
+    // full and at light load when every image chunk is gathered element by
+    // element; < 0 if not measured
+    double step_gather, step_gather_light;
 };
 // Calibration of a kernel, or nullptr when none is loaded / it is disabled.
 const VxCalib* vxi_calib(int kernel_id);
@@ -47,6 +51,10 @@ struct VxShape {
     int c_vec;     // C allows 4-element vector stores
     int op = 0;    // 0: GEMM; 1: 2-D convolution as an implicit GEMM (conv kernels only)
     int64_t a_bytes = 0;   // convolution: bytes of the image (the direct-to-LDS kernels need < 2^31)
+    // convolution: the share of the image's 16-byte chunks that the kernels
+    // gathering the image through VGPRs load element by element (0 when the
+    // channels come in whole chunks)
+    double gather_frac = 0.0;
 };
 
 struct VxLimits {

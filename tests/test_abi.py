@@ -427,15 +427,44 @@ def test_conv2d_extent_limits(mi355x_override):
 
 
 def test_conv2d_large_image_avoids_32_bit_offsets(mi355x_override):
-    """An image of 2^31 bytes or more is beyond the direct-to-LDS kernels'
-    32-bit buffer offsets: the plan takes a register-staged kernel, which
-    forms 64-bit addresses; below that a direct-to-LDS kernel is planned."""
+    """An image of 2^31 bytes or more is beyond the direct-to-LDS image
+    loads' 32-bit buffer offsets: the plan takes a kernel that gathers the
+    image through VGPRs with 64-bit addresses (register-staged, or mixed with
+    the filter by DMA); below that a direct-to-LDS kernel is planned."""
     big = vx.conv_desc(1, 1 << 15, 1 << 12, 16, 8, 1, 1, vx.VX_F16)      # 2^31 elements, 2^32 bytes
     p = vx.vx_conv2d_plan_query(big)
-    assert p.kernel.op == 1 and p.kernel.family == 0
+    assert p.kernel.op == 1 and (p.kernel.family == 0 or not p.kernel.align & 1)
     small = vx.conv_desc(8, 256, 256, 64, 128, 3, 3, vx.VX_F16, pad=(1, 1))
     p = vx.vx_conv2d_plan_query(small)
     assert p.kernel.op == 1 and p.kernel.family == 1
+
+
+def test_conv_element_gathers_priced(mi355x_override):
+    """Three convolutions with the same implicit GEMM (M = 1024, N = 64,
+    K = 72): a 1 x 1 filter over 72 channels (whole 16-byte chunks), an 8 x 3
+    filter over 3 channels (7 of every 9 chunk positions cross the end of a
+    filter row and are gathered element by element), and an 8 x 9 filter over
+    one channel dilated 2 along the width (every chunk gathered).  With the
+    shipped calibration, a kernel that gathers the image through VGPRs is
+    priced by that share: the cost grows with it, linearly (the same grid),
+    and the three shapes are planned apart (the plan cache tells them
+    apart)."""
+    shapes = {"whole": vx.conv_desc(1, 32, 32, 72, 64, 1, 1, vx.VX_F16),
+              "part": vx.conv_desc(1, 39, 34, 3, 64, 8, 3, vx.VX_F16),
+              "all": vx.conv_desc(1, 39, 48, 1, 64, 8, 9, vx.VX_F16, dil=(1, 2))}
+    ks = [vx.vx_registry_get(i) for i in range(vx.vx_registry_count())]
+    k = next(k for k in ks if k.op == 1 and k.dtype == 1 and k.enabled and not k.align & 1)
+    cost = {}
+    for name, d in shapes.items():
+        assert vx.vx_force_plan(k.id, 1) == 0
+        try:
+            p = vx.vx_conv2d_plan_query(d)
+        finally:
+            vx.vx_force_plan(-1, 0)
+        assert p.kernel_id == k.id and (p.tiles_m, p.tiles_n) == (-(-1024 // k.mb), -(-64 // k.nb))
+        cost[name] = p.predicted_ns
+    assert cost["whole"] < cost["part"] < cost["all"]
+    assert cost["part"] - cost["whole"] == pytest.approx(7.0 / 9.0 * (cost["all"] - cost["whole"]), rel=1e-6)
 
 
 def test_hybrid_grid_plans(mi355x_override):

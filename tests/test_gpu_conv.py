@@ -55,8 +55,8 @@ def test_every_conv_kernel_integer_exact(code):
     assert ks
     for k in ks:
         # the direct-to-LDS kernels take channel counts that are multiples of 8
-        for Cin in ((8, 24) if k.vec else (3, 8)):
-            Cout = k.nb + (8 if k.vec else 5)
+        for Cin in ((8, 24) if k.align & 1 else (3, 8)):   # image by DMA: channels in 16-byte chunks
+            Cout = k.nb + (8 if k.align & 2 else 5)          # filter by DMA: rows of 16-byte chunks
             N, H, W, KH, KW, st, pd, dl = 2, 11, 10, 3, 3, (2, 1), (1, 2), (1, 2)
             x = I.small_int(g, (N, H, W, Cin), code, -3, 3)
             w = I.small_int(g, (KH, KW, Cin, Cout), code, -3, 3)
@@ -71,19 +71,21 @@ def test_every_conv_kernel_integer_exact(code):
 
 @pytest.mark.parametrize("code", DTS)
 def test_every_register_conv_kernel_contiguous_taps(code):
-    """The register-staged convolution kernels with channel counts that are not
-    multiples of the 16-byte chunk and unit dilation along the width: chunks
-    that stay inside one filter row load as one vector, chunks across a filter
-    row's end, on padding or past K are gathered element by element.  A 3 x 5
-    filter with c_in 3, 5 and 12 puts chunk boundaries at every position of a
-    row; small integers make every result exact."""
+    """The convolution kernels that gather the image through VGPRs (the
+    register-staged ones, and the mixed ones that take the filter by DMA) with
+    channel counts that are not multiples of the 16-byte chunk and unit
+    dilation along the width: chunks that stay inside one filter row load as
+    one vector, chunks across a filter row's end, on padding or past K are
+    gathered element by element.  A 3 x 5 filter with c_in 3, 5 and 12 puts
+    chunk boundaries at every position of a row; small integers make every
+    result exact."""
     g = I.rng(1250 + code)
     ks = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count()))
-          if k.op == 1 and k.dtype == code and k.enabled and not k.vec]
+          if k.op == 1 and k.dtype == code and k.enabled and not k.align & 1]
     assert ks
     for k in ks:
         for Cin in (3, 5, 12):
-            Cout = k.nb + 5
+            Cout = k.nb + (8 if k.align & 2 else 5)
             N, H, W, KH, KW, st, pd, dl = 2, 11, 13, 3, 5, (1, 2), (2, 1), (2, 1)
             x = I.small_int(g, (N, H, W, Cin), code, -3, 3)
             w = I.small_int(g, (KH, KW, Cin, Cout), code, -3, 3)
@@ -101,21 +103,22 @@ def test_conv_split_k_integer_exact(code):
     g = I.rng(1300 + code)
     conv = [k for k in (vx.vx_registry_get(i) for i in range(vx.vx_registry_count()))
             if k.op == 1 and k.dtype == code and k.enabled]
-    N, H, W, Cin, Cout, KH, KW = 1, 9, 9, 40, 24, 3, 3
-    x = I.small_int(g, (N, H, W, Cin), code, -2, 2)
-    w = I.small_int(g, (KH, KW, Cin, Cout), code, -2, 2)
-    ref = oracle.conv2d(x, w, code, (1, 1), (1, 1), (1, 1), with_mag=False)
+    N, H, W, Cout, KH, KW = 1, 9, 9, 24, 3, 3
     firsts = {}
     for k in conv:
-        firsts.setdefault(k.family, k)
+        firsts.setdefault((k.family, k.align), k)
     for k, split in ((k, s) for k in firsts.values() for s in (2, 3)):
+        Cin = 40 if k.align & 1 else 37   # channels in whole chunks only where the image is DMA'd
+        x = I.small_int(g, (N, H, W, Cin), code, -2, 2)
+        w = I.small_int(g, (KH, KW, Cin, Cout), code, -2, 2)
+        ref = oracle.conv2d(x, w, code, (1, 1), (1, 1), (1, 1), with_mag=False)
         assert vx.vx_force_plan(k.id, split) == 0
         try:
             y1 = run_conv(x, w, code, (1, 1), (1, 1), (1, 1))
             y2 = run_conv(x, w, code, (1, 1), (1, 1), (1, 1))
         finally:
             vx.vx_force_plan(-1, 0)
-        tolerance.check_exact(y1, ref, code, "conv split %d" % split)
+        tolerance.check_exact(y1, ref, code, "conv kernel %d split %d" % (k.id, split))
         assert np.array_equal(y1, y2)
 
 
