@@ -250,13 +250,21 @@ def _entry(dtype, family, stages, c, vec, hw):
 CONV_TILES = {(32, 32), (32, 64), (64, 32), (64, 64), (64, 128), (128, 64), (128, 128)}
 
 
-def conv_candidates(dtype, hw=GFX950):
+# Tiles of at most 64 x 64 also come with three register sets of K steps in
+# flight (stages = 4: the register sets plus the LDS stage being computed):
+# a small layer with few workgroups and few K steps (a first layer over three
+# channels: K = 147, three steps) otherwise waits one gather round trip per
+# K step.
+CONV_PF_TILES = {(32, 32), (32, 64), (64, 32), (64, 64)}
+
+
+def conv_candidates(dtype, hw=GFX950, pf=False):
     kb = 64 if ELEM_BYTES[dtype] == 2 else 32
     out = []
     for c in workgroup_tiles(dtype, hw, "reg"):
         mb, nb, ckb, wm, wn, mi = c
-        if ckb == kb and (mb, nb) in CONV_TILES and wm * wn == 4:
-            e = _entry(dtype, "reg", 2, c, 0, hw)
+        if ckb == kb and (mb, nb) in CONV_TILES and wm * wn == 4 and (not pf or (mb, nb) in CONV_PF_TILES):
+            e = _entry(dtype, "reg", 4 if pf else 2, c, 0, hw)
             e["op"] = 1
             out.append(e)
     return out
@@ -461,6 +469,8 @@ def registry(hw=GFX950):
         out += short_k_candidates(dtype, hw)
     for dtype in ("f16", "bf16"):
         out += conv_mixed_candidates(dtype, hw)
+    for dtype in ("f16", "bf16", "f32"):
+        out += conv_candidates(dtype, hw, pf=True)
     for i, e in enumerate(out):
         e["id"] = i
     return out

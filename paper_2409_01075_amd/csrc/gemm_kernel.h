@@ -65,11 +65,14 @@ enum { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
 // WM x WN wavefronts, MFMA instruction tile MI x MI, operands whose rows are
 // 16-byte aligned (VEC) or only element aligned, and whether A is a plain
 // matrix or a convolution's input image (CONV: the implicit GEMM).
-template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, bool VEC_, bool CONV_ = false>
+template <int DT_, int MB_, int NB_, int KB_, int WM_, int WN_, int MI_, bool VEC_, bool CONV_ = false, int PF_ = 1>
 struct Cfg {
     static constexpr int DT = DT_, MB = MB_, NB = NB_, KB = KB_, WM = WM_, WN = WN_, MI = MI_;
     static constexpr bool VEC = VEC_;
     static constexpr bool CONV = CONV_;                  // A is an image read through the im2col map
+    // K steps whose loads are in flight in registers while one step computes
+    // from LDS (PF register sets; the LDS keeps its two stages)
+    static constexpr int PF = PF_;
     static constexpr bool H = DT != DT_F32;              // 16-bit inputs
     static constexpr int NT = WM * WN * 64;              // threads per workgroup
     static constexpr int MW = MB / WM, NW = NB / WN;     // wavefront tile
@@ -107,6 +110,7 @@ struct Cfg {
     static_assert(BV >= 1 && (H ? BV * 8 : BV * 4) * NT == NB * KB, "B tile must split evenly over threads");
     static_assert(!H || (BBLK >= 1 && BBLK * NT * BK * 8 == KB * NB), "B blocks must split evenly");
     static_assert(LDS_BYTES <= 159 * 1024, "LDS budget of one CU, less 1 KiB for the split-K flag");
+    static_assert(PF >= 1 && PF <= 4, "register sets of K steps in flight");
 };
 
 __device__ __forceinline__ unsigned lo16(unsigned w) { return w & 0xffffu; }
@@ -917,32 +921,44 @@ __device__ __forceinline__ void gemm_body(const VxGemmArgs& args)
     Acc<C> acc;
     acc_zero<C>(acc);
 
-    Tile<C> tl;
+    // PF register sets: set j holds K steps j, j + PF, j + 2 PF, ... on their
+    // way from memory into the LDS stage; the loop is unrolled by PF so that
+    // every set index is a constant
+    Tile<C> tl[C::PF];
     ConvA<C> ca;
     if constexpr (C::CONV)
         ca.init(p, g.m0, g.kbeg, t);
-    // one K step of A and B into registers (for a convolution, A through the
-    // im2col map; the steps come in order, so its state just advances)
-    auto load = [&](int k0) {
-        tl.load(Ab, Bb, 0, g.n0, k0, g.kend, Mrel, p.N, p.K, t);
+    // one K step of A and B into register set s (for a convolution, A through
+    // the im2col map; the steps are loaded in order, so its state just advances)
+    auto load = [&](Tile<C>& s, int k0) {
+        s.load(Ab, Bb, 0, g.n0, k0, g.kend, Mrel, p.N, p.K, t);
         if constexpr (C::CONV) {
-            tl.load_a_conv(p, (const char*)p.A, ca, g.kend);
+            s.load_a_conv(p, (const char*)p.A, ca, g.kend);
             ca.advance(p);
         }
     };
-    if (g.nk > 0) {
-        load(g.kbeg);
-        tl.store(smem, t);
-    }
+#pragma unroll
+    for (int j = 0; j < C::PF; ++j)
+        if (j < g.nk)
+            load(tl[j], g.kbeg + j * C::KB);
+    if (g.nk > 0)
+        tl[0].store(smem, t);
     __syncthreads();
-    for (int it = 0; it < g.nk; ++it) {
-        char* cur = smem + (it & 1) * C::STAGE_BYTES;
-        if (it + 1 < g.nk)
-            load(g.kbeg + (it + 1) * C::KB);
-        compute_step<C>(cur, acc, wm0, wn0, lane);
-        if (it + 1 < g.nk)
-            tl.store(smem + ((it + 1) & 1) * C::STAGE_BYTES, t);
-        __syncthreads();
+    for (int it0 = 0; it0 < g.nk; it0 += C::PF) {
+#pragma unroll
+        for (int j = 0; j < C::PF; ++j) {
+            const int it = it0 + j;
+            if (it >= g.nk)
+                break;
+            char* cur = smem + (it & 1) * C::STAGE_BYTES;
+            // set j held step it, already in LDS: it takes step it + PF
+            if (it + C::PF < g.nk)
+                load(tl[j], g.kbeg + (it + C::PF) * C::KB);
+            compute_step<C>(cur, acc, wm0, wn0, lane);
+            if (it + 1 < g.nk)
+                tl[(j + 1) % C::PF].store(smem + ((it + 1) & 1) * C::STAGE_BYTES, t);
+            __syncthreads();
+        }
     }
     // the loop ends with a barrier: LDS is idle here
     if (g.split > 1 && !reduce_split<C>(p, acc, g, t))
