@@ -90,15 +90,6 @@ inline bool kernel_fits(const VxShape& sh, const vx_kernel_info& k, bool hyb, in
 {
     if (k.k_max > 0 && (hyb ? sh.K : kps) > k.k_max)   // the kernel holds a whole slice of A in LDS
         return false;
-    // The mixed im2col tiles (image through VGPRs, filter by DMA) carry one K
-    // step of image gathers at a time; where a quarter or more of the image's
-    // chunks are gathered element by element (first layers over a few channels)
-    // they ran 1.3-1.7x slower than the register-staged tiles, and the
-    // calibrated step costs (whole-chunk and fully gathered steps) priced
-    // them 30-40 % low there (stem layers: 11.2-11.8 us measured, 8.1-8.4
-    // predicted).  They are offered only below that share.
-    if (k.op == 1 && k.family == 1 && !(k.align & 1) && sh.gather_frac >= 0.25)
-        return false;
     const int eb = sh.dt == VX_F32 ? 4 : 2;
     if (k.family == 1) {
         // direct-to-LDS kernels address each K step with 32-bit buffer offsets:
@@ -609,6 +600,16 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
     auto beaten = [&](double lb) { return prune && lb > best.cost * (1.0 + 1e-9); };
     auto admitted = [&](const vx_kernel_info& k) {
         if ((forced_id >= 0 && k.id != forced_id) || !vxi_wave_matches(f, k))
+            return false;
+        // The mixed im2col tiles (image through VGPRs, filter by DMA) carry one
+        // K step of image gathers at a time; where a quarter or more of the
+        // image's chunks are gathered element by element (first layers over a
+        // few channels) they ran 1.3-1.7x slower than the register-staged
+        // tiles, and the calibrated step costs (whole-chunk and fully gathered
+        // steps) priced them 30-40 % low there (stem layers: 11.2-11.8 us
+        // measured, 8.1-8.4 predicted).  The selector offers them only below
+        // that share; a forced plan may still take them.
+        if (forced_id < 0 && k.op == 1 && k.family == 1 && !(k.align & 1) && sh.gather_frac >= 0.25)
             return false;
         return (f.backends & (k.family == 2 ? 2 : 1)) && !(k.align & ~sh.vec_ok);
     };
