@@ -20,7 +20,8 @@ time in the sweep: its algorithmic bytes per launch (the compulsory
 (M*K + K*N + M*N)*2 bytes) over its average event-timed duration, against the
 8 TB/s HBM peak (every sweep shape is below the fp16 ridge point of 314.6
 FLOP/byte).  cpu_baseline times the CPU oracle on a bounded subset of the
-same shapes on this host's cores.
+same shapes on this host's cores, then checks (untimed) sampled outputs of the
+timed back-to-back pass for every M against the oracle.
 
 Beside the sweep the same run reports: launch_floor_us, the back-to-back
 device time of an empty kernel (the dispatch floor every sweep shape sits on:
@@ -168,7 +169,7 @@ def _cpu_model():
     return None
 
 
-def _cpu_baseline(ms, budget_s):
+def _cpu_baseline(ms, budget_s, outputs=None):
     """Times the CPU oracle (as it stands) on a bounded subset of the sweep."""
     import numpy as np
     import oracle
@@ -187,12 +188,44 @@ def _cpu_baseline(ms, budget_s):
         if time.perf_counter() - t_all > budget_s:
             break
     geo = math.exp(sum(math.log(r) for r in rates) / len(rates))
-    return {"value": geo, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+    res = {"value": geo, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "affinity_cpus": _affinity_cpus(), "cpu_model": _cpu_model(),
             "sample": "fp16 sweep shapes M in %s (every 8th M from 1, %d shapes, full outputs, "
                       "fp64 accumulation, decode included), geomean over the sample; threads = the "
                       "process's CPUs, at most 16 (one GPU's share of the host)"
                       % ("{%d..%d}" % (done[0], done[-1]), len(done))}
+    if outputs is not None:
+        res["outputs_checked"] = _check_outputs(ms, outputs, threads)
+    return res
+
+
+def _check_outputs(ms, outputs, threads, n_rand=512):
+    """The sweep's outputs from the timed back-to-back pass, checked (untimed)
+    against the oracle's fp64 values at sampled positions of every M: the
+    whole last row and last column plus n_rand seeded random entries, each a
+    full-K dot product, under the fp16 bound |C - Cref| <= 4e-3 Mag + 1e-6."""
+    import numpy as np
+    import oracle
+    from oracle import tolerance
+    from paper_2409_01075_amd import inputs as I
+    g = I.rng(7000)
+    worst, bad, n = 0.0, None, 0
+    for M in ms:
+        A, B = I.sweep_f16(M, K_SWEEP, N_SWEEP)
+        rows = np.concatenate([np.full(N_SWEEP, M - 1), np.arange(M), g.integers(0, M, n_rand)])
+        cols = np.concatenate([np.arange(N_SWEEP), np.full(M, N_SWEEP - 1), g.integers(0, N_SWEEP, n_rand)])
+        ref, mag = oracle.gemm_sampled(A, B, I.F16, M, N_SWEEP, K_SWEEP, rows, cols, threads=threads)
+        n += rows.size
+        try:
+            worst = max(worst, tolerance.check(outputs[M][rows, cols], ref, mag, I.F16, "sweep M=%d" % M))
+        except AssertionError as e:
+            bad = bad or str(e)
+    out = {"shapes": len(ms), "entries": n, "max_err_over_bound": worst, "within_bound": bad is None,
+           "sample": "every sweep M: last row, last column and %d random entries of the timed "
+                     "back-to-back pass's C, oracle fp64 dot products" % n_rand}
+    if bad is not None:
+        out["first_failure"] = bad
+    return out
 
 
 def _set_jobs(name, trials, shapes="", dtype="bf16"):
@@ -465,6 +498,10 @@ def run_study(args):
             json.dump(rows, f)
     out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
+    chk = out.get("cpu_baseline", {}).get("outputs_checked")
+    if chk is not None and not chk["within_bound"]:
+        print("sweep outputs outside the bound: %s" % chk.get("first_failure"), file=sys.stderr, flush=True)
+        sys.exit(3)
 
 
 def run_adapt(args):
@@ -657,6 +694,10 @@ def run_conv(args):
             json.dump(results, f)
     out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
+    chk = out.get("cpu_baseline", {}).get("outputs_checked")
+    if chk is not None and not chk["within_bound"]:
+        print("sweep outputs outside the bound: %s" % chk.get("first_failure"), file=sys.stderr, flush=True)
+        sys.exit(3)
 
 
 def _device_warmup(dev, ms=150.0):
@@ -842,6 +883,10 @@ def run_set(args):
             json.dump(results, f)
     out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
+    chk = out.get("cpu_baseline", {}).get("outputs_checked")
+    if chk is not None and not chk["within_bound"]:
+        print("sweep outputs outside the bound: %s" % chk.get("first_failure"), file=sys.stderr, flush=True)
+        sys.exit(3)
 
 
 def _launch_floor_us(stream, reps=3, n=400):
@@ -1020,6 +1065,10 @@ def main():
         torch.cuda.synchronize()
         pass_ms.append(e0.elapsed_time(e1))
 
+    # the outputs of the last timed pass, for the oracle's check in the CPU leg
+    host_c = None if args.no_cpu_baseline else \
+        {M: Ct.view(torch.int16).cpu().numpy().view(np.uint16) for (M, _, _, Ct) in sets}
+
     # the dispatch floor beside the sweep (every sweep shape's roofline time is below 5 us)
     launch_floor = _launch_floor_us(stream)
     k0_call = _k0_call_us(stream, L)
@@ -1088,7 +1137,7 @@ def main():
     if sets_out:
         out["sets"] = sets_out
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = _cpu_baseline(ms, args.cpu_seconds)
+        out["cpu_baseline"] = _cpu_baseline(ms, args.cpu_seconds, host_c)
     if args.detail:
         with open(args.detail, "w") as f:
             json.dump({"M": ms, "ms": med.tolist(), "tflops": tflops.tolist(),
@@ -1097,6 +1146,10 @@ def main():
                       f)
     out["selector"] = _selector_kind()
     print(json.dumps(out), flush=True)
+    chk = out.get("cpu_baseline", {}).get("outputs_checked")
+    if chk is not None and not chk["within_bound"]:
+        print("sweep outputs outside the bound: %s" % chk.get("first_failure"), file=sys.stderr, flush=True)
+        sys.exit(3)
 
 
 if __name__ == "__main__":
