@@ -326,13 +326,18 @@ bool vxi_wave_matches(const VxFilter& f, const vx_kernel_info& k)
 //   cost >= launch + max(floor, (F - 1)(fix_full + nk_s step_full)
 //                                + fix_min + nk_s step_min + epilogue).
 // Over all splits: the K steps one slot runs add up to X >= max(T, 1), T =
-// tiles nk / S (nk = ceil(K/Kb)), the last wave runs at most nk of them, so
-// the steps cost >= max(0, X - nk) step_full + min(X, nk) step_min; with the
-// epilogue growing in s, a split whose bound is beaten ends the split loop.
-// A group's bound over its plans with s >= 2: the steps of s_max with the
-// epilogue of s = 2 (weak), or step_min max(T, nk / s) + a + b (s - 1), a
-// convex function of a real s least at s = sqrt(step_min nk / b) clamped to
-// [2, s_max] and to at most nk / T (tight).  A group's terms are the least of
+// tiles nk / S (nk = ceil(K/Kb)), the last wave runs at most nk_s of them
+// (nk_s = the steps of one of s slices, never more at a larger split), so the
+// steps cost >= max(0, X - nk_s) step_full + min(X, nk_s) step_min; a plan of
+// s >= 2 slices also runs >= floor(tiles / S) waves before its last, each
+// with the full-load fixed time; with the epilogue growing in s, a split
+// whose bound is beaten ends the split loop, and so does one where
+// step_min max(T, nk / s') + a + b (s' - 1), convex in a real s', is beaten
+// at its least over s' >= s.  A group's bound over its plans with s >= 2:
+// the steps of s_max with the epilogue of s = 2 (weak), or the greater of
+// step_min max(T, nk / s) + a + b (s - 1) at the real s = sqrt(step_min nk /
+// b) clamped to [2, s_max] and to at most nk / T, and the step bound above
+// with nk_2 and the epilogue a + b (tight).  A group's terms are the least of
 // its kernels' (each bound grows with every term).  Uncalibrated kernels are
 // bounded by launch + floor only.
 
@@ -573,24 +578,34 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
         const int64_t f = (int64_t)((double)a * inv_b);
         return f + (f * b < a ? 1 : 0);
     };
-    // least K steps per slice over every split the search takes, and sqrt(nk), per Kb
-    int64_t nk_smax[kMaxExtents];
+    // least K steps per slice over every split the search takes, the most over
+    // splits >= 2 (those of two slices), and sqrt(nk), per Kb
+    int64_t nk_smax[kMaxExtents], nk_half[kMaxExtents];
     double sq_nk[kMaxExtents];
     for (int i = 0; i < CL.n_kb; ++i) {
         nk_smax[i] = std::max<int64_t>(1, ceil_div(ck[i], (int64_t)s_max));
+        nk_half[i] = K0 ? 0 : cdiv(kcut[1], CL.kb[i]);
         sq_nk[i] = sqrt((double)ck[i]);
     }
+    // the K steps of a slot that runs X in all, at most `last` of them in the
+    // last wave (at no less than step_min), the others at step_full
+    auto steps_lo = [](const BoundTerms& b, double X, double last) {
+        return std::max(0.0, X - last) * b.step_full + std::min(X, last) * b.step_min;
+    };
     // a group's bound over its plans with s >= 2 slices: steps per slot >=
     // max(T, nk / s), epilogue >= a + b (s - 1); as a function of a real s this
     // is convex, least at s = sqrt(step_min nk / b), clamped to [2, s_max] and
-    // to <= nk / T
-    auto many_tight = [&](const BoundTerms& b, int64_t tiles, int64_t nkw, double sqnk) {
+    // to <= nk / T.  Or: the slot's max(T, 1) steps but the last wave's (at
+    // most those of two slices, nk2) at the full-load step, epilogue >= a + b
+    auto many_tight = [&](const BoundTerms& b, int64_t tiles, int64_t nkw, double sqnk, int64_t fdp, int64_t nk2) {
         const double nk = (double)nkw, Tq = (double)tiles * nk * b.inv_slots;
         double s = b.split_b > 0.0 ? b.c_split * sqnk : s_max;
         if (Tq > 0.0 && s * Tq > nk)
             s = nk / Tq;
         s = std::min(std::max(s, 2.0), std::max(s_max, 2.0));
-        return b.fix_min + b.step_min * std::max(Tq, nk / s) + b.split_a + b.split_b * (s - 1.0);
+        const double convex = b.step_min * std::max(Tq, nk / s) + b.split_b * (s - 1.0);
+        const double waves = steps_lo(b, std::max(Tq, 1.0), (double)nk2) + b.split_b;
+        return b.fix_min + (double)fdp * b.fix_full + b.split_a + std::max(convex, waves);
     };
 
     auto lb_of = [&](double lo, bool cal) {
@@ -650,15 +665,20 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
     auto price_group = [&](const SelGroup& g, int64_t tiles, int64_t nk_whole) {
         const bool ext = g.ki >= 0;
         const BoundTerms& b = g.bt;
+        const int64_t Fdp = tiles / b.slots;
         if (b.cal && prune && forced_split == 0 && !K0 && nk_whole >= 2) {
             // the group passed its weak bound; the tight one over every split
             const double one = b.lo(std::max<int64_t>(1, ceil_mul(tiles, b.slots, b.inv_slots)), (double)nk_whole, 1);
-            if (beaten(lb_of(std::min(one, many_tight(b, tiles, nk_whole, ext ? sq_nk[g.ki] : sqrt((double)nk_whole))),
-                             true)))
+            const double sq = ext ? sq_nk[g.ki] : sqrt((double)nk_whole);
+            const int64_t nk2 = ext ? nk_half[g.ki] : cdiv(kcut[1], g.kb);
+            if (beaten(lb_of(std::min(one, many_tight(b, tiles, nk_whole, sq, Fdp, nk2)), true)))
                 return;
         }
-        const int64_t Fdp = tiles / b.slots;
         const double Tq = (double)tiles * (double)nk_whole * b.inv_slots;   // K steps per slot, whole grid
+        // a plan of s >= 2 slices runs >= floor(tiles / slots) waves before its
+        // last (plain grid: ceil(s tiles / slots) - 1; hybrid: that many whole
+        // waves), each at the full-load fixed time
+        const double fix_waves = (double)Fdp * b.fix_full;
         if (forced_split != 0) {
             // a forced split runs as the number of non-empty slices it yields
             const int fs = forced_split < 0 ? -forced_split : forced_split;
@@ -691,12 +711,25 @@ vx_status vxi_select(const vx_hwinfo& hw, const VxShape& sh, const VxLimits& lim
                 continue;   // a slice would be empty
             if (b.cal && prune && split > 1) {
                 // every split's slots run >= max(T, 1) K steps in all, the last
-                // wave at most nk_whole of them, and the epilogue grows with the
-                // split: once that is beaten, every larger split is
+                // wave at most this split's nk of them (a larger split's slices
+                // are no longer), and the epilogue grows with the split: once
+                // that is beaten, every larger split is
                 const double X = std::max(Tq, 1.0), nkw = (double)nk_whole;
-                const double steps = std::max(0.0, X - nkw) * b.step_full + std::min(X, nkw) * b.step_min;
-                if (beaten(lb_of(b.fix_min + steps + b.split_a + b.split_b * (double)(split - 1), true)))
+                const double steps = steps_lo(b, X, (double)nk);
+                if (beaten(lb_of(b.fix_min + fix_waves + steps + b.split_a + b.split_b * (double)(split - 1), true)))
                     break;
+                // ... and a slot of s' >= split slices runs >= nk_whole / s'
+                // steps too: step_min max(T, nk / s') + a + b (s' - 1) is
+                // convex in a real s', least over s' >= split at max(split, s*)
+                if (b.split_b > 0.0) {
+                    double sr = b.c_split * (ext ? sq_nk[g.ki] : sqrt(nkw));
+                    if (Tq > 0.0 && sr * Tq > nkw)
+                        sr = nkw / Tq;
+                    sr = std::max(sr, (double)split);
+                    if (beaten(lb_of(b.fix_min + fix_waves + b.step_min * std::max(Tq, nkw / sr) + b.split_a +
+                                         b.split_b * (sr - 1.0), true)))
+                        break;
+                }
             }
             // plain grid
             const int64_t Fg = std::max<int64_t>(1, ceil_mul(tiles * split, b.slots, b.inv_slots));
